@@ -1,0 +1,179 @@
+"""Seeded synthetic inputs for the Gated DeltaNet decode and varlen-prefill paths.
+
+This module only draws numbers; it holds none of the recurrence's arithmetic.
+Both the CPU oracle (through the tests) and the HIP path (through the binding,
+the tests and the benchmark) take their inputs from here, so the two sides see
+bit-identical operands.
+
+Distributions follow the workload descriptions used throughout the build:
+  q, k : N(0, 1) in fp32, L2-normalised over the head dimension, then rounded
+         to bf16 (round-to-nearest-even).  The kernels do not normalise.
+  v    : N(0, 1) rounded to bf16.
+  beta : sigmoid(N(0, 1)) in fp32, i.e. post-sigmoid write strength in (0, 1).
+  g    : -softplus(N(0, 1)) in fp32, the natural-log gate; alpha = exp(g).
+  state: 0.02 * N(0, 1) in fp32 (std 0.02), or zeros where a workload says so.
+
+bf16 tensors are returned as numpy ``uint16`` arrays holding the raw bit
+patterns; :func:`to_torch` turns them into ``torch.bfloat16`` tensors without
+changing a bit.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Optional, Sequence
+
+import numpy as np
+
+__all__ = [
+    "bf16_bits",
+    "DecodeInputs",
+    "PrefillInputs",
+    "decode_inputs",
+    "prefill_inputs",
+    "varlen_lengths",
+    "WORKLOADS",
+    "to_torch",
+]
+
+
+def bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round fp32 values to bf16 (nearest, ties to even); return the uint16 bit patterns.
+
+    NaN is not produced by the generators and is not handled specially.
+    """
+    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    rounded = (b + np.uint32(0x7FFF) + ((b >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    return rounded.astype(np.uint16)
+
+
+def _rng(seed: int) -> np.random.Generator:
+    return np.random.Generator(np.random.Philox(seed))
+
+
+def _unit_rows(rng: np.random.Generator, shape) -> np.ndarray:
+    x = rng.standard_normal(shape, dtype=np.float32)
+    x /= np.linalg.norm(x, axis=-1, keepdims=True)
+    return x
+
+
+def _softplus(x: np.ndarray) -> np.ndarray:
+    return np.logaddexp(np.float32(0.0), x).astype(np.float32)
+
+
+def _sigmoid(x: np.ndarray) -> np.ndarray:
+    return (1.0 / (1.0 + np.exp(-x))).astype(np.float32)
+
+
+@dataclasses.dataclass
+class DecodeInputs:
+    """One decode step: q, k [B, H_qk, D] bf16 bits; v [B, H_v, D] bf16 bits;
+    g, beta [B, H_v] fp32; state [B, H_v, D_v, D_k] fp32 (k index contiguous)."""
+
+    q: np.ndarray
+    k: np.ndarray
+    v: np.ndarray
+    g: np.ndarray
+    beta: np.ndarray
+    state: np.ndarray
+    scale: float = 1.0
+
+    @property
+    def shape(self):
+        B, H_qk, D = self.q.shape
+        return B, H_qk, self.v.shape[1], D
+
+
+@dataclasses.dataclass
+class PrefillInputs:
+    """Packed varlen prefill: q, k [T, H_qk, D] bf16 bits; v [T, H_v, D] bf16 bits;
+    g, beta [T, H_v] fp32; cu_seqlens int32 [N + 1]; initial_state fp32
+    [N, H_v, D_v, D_k] or None (zero state)."""
+
+    q: np.ndarray
+    k: np.ndarray
+    v: np.ndarray
+    g: np.ndarray
+    beta: np.ndarray
+    cu_seqlens: np.ndarray
+    initial_state: Optional[np.ndarray]
+    scale: float = 1.0
+
+    @property
+    def shape(self):
+        T, H_qk, D = self.q.shape
+        return len(self.cu_seqlens) - 1, T, H_qk, self.v.shape[1], D
+
+
+def decode_inputs(seed: int, B: int, H_qk: int, H_v: int, D: int,
+                  state_std: float = 0.02, scale: float = 1.0,
+                  qkv_dtype: str = "bf16") -> DecodeInputs:
+    """Draw one decode step.  ``qkv_dtype="f32"`` keeps q/k/v as fp32 (oracle-only use)."""
+    rng = _rng(seed)
+    q = _unit_rows(rng, (B, H_qk, D))
+    k = _unit_rows(rng, (B, H_qk, D))
+    v = rng.standard_normal((B, H_v, D), dtype=np.float32)
+    beta = _sigmoid(rng.standard_normal((B, H_v), dtype=np.float32))
+    g = -_softplus(rng.standard_normal((B, H_v), dtype=np.float32))
+    if state_std == 0.0:
+        state = np.zeros((B, H_v, D, D), np.float32)
+    else:
+        state = (np.float32(state_std) * rng.standard_normal((B, H_v, D, D), dtype=np.float32))
+    if qkv_dtype == "bf16":
+        q, k, v = bf16_bits(q), bf16_bits(k), bf16_bits(v)
+    return DecodeInputs(q, k, v, g, beta, state, scale)
+
+
+def varlen_lengths(seed: int, N: int, lo: int, hi: int) -> np.ndarray:
+    """N sequence lengths drawn uniformly from the integers in [lo, hi]."""
+    return _rng(seed + 7919).integers(lo, hi + 1, size=N).astype(np.int64)
+
+
+def prefill_inputs(seed: int, lengths: Sequence[int], H_qk: int, H_v: int, D: int,
+                   state_std: Optional[float] = None, scale: float = 1.0,
+                   qkv_dtype: str = "bf16") -> PrefillInputs:
+    """Draw a packed varlen batch.  ``state_std=None`` means a zero initial state
+    (passed to the library as NULL)."""
+    lengths = np.asarray(lengths, dtype=np.int64)
+    N = len(lengths)
+    cu = np.zeros(N + 1, np.int64)
+    np.cumsum(lengths, out=cu[1:])
+    T = int(cu[-1])
+    rng = _rng(seed)
+    q = _unit_rows(rng, (T, H_qk, D))
+    k = _unit_rows(rng, (T, H_qk, D))
+    v = rng.standard_normal((T, H_v, D), dtype=np.float32)
+    beta = _sigmoid(rng.standard_normal((T, H_v), dtype=np.float32))
+    g = -_softplus(rng.standard_normal((T, H_v), dtype=np.float32))
+    init = None
+    if state_std is not None:
+        init = (np.float32(state_std) * rng.standard_normal((N, H_v, D, D), dtype=np.float32))
+    if qkv_dtype == "bf16":
+        q, k, v = bf16_bits(q), bf16_bits(k), bf16_bits(v)
+    return PrefillInputs(q, k, v, g, beta, cu.astype(np.int32), init, scale)
+
+
+# The five synthetic workloads (sizes and distributions as described in the
+# module docstring).  Values are plain dicts so both sides can read them.
+WORKLOADS = {
+    "tiny": dict(kind="both", N=1, T=64, H_qk=2, H_v=2, D=16, chunk=16, state_std=None, seed=1),
+    "decode_b64": dict(kind="decode", B=64, H_qk=16, H_v=32, D=128, state_std=0.02, seed=2),
+    "decode_sweep": dict(kind="decode", batches=(1, 8, 256, 1024), steps=100, H_qk=16, H_v=32,
+                         D=128, state_std=0.02, seed=3),
+    "prefill_varlen16": dict(kind="prefill", N=16, len_lo=128, len_hi=2048, H_qk=16, H_v=32,
+                             D=128, chunk=64, state_std=None, seed=4),
+    "prefill_long2x64k": dict(kind="prefill", N=2, len=65536, H_qk=16, H_v=32, D=128, chunk=64,
+                              state_std=0.02, seed=5),
+}
+
+
+def to_torch(x: Optional[np.ndarray], device=None, bf16: bool = False):
+    """numpy -> torch on ``device``; uint16 bf16 bit patterns become torch.bfloat16."""
+    import torch
+
+    if x is None:
+        return None
+    if bf16:
+        t = torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16)
+    else:
+        t = torch.from_numpy(np.ascontiguousarray(x))
+    return t.to(device) if device is not None else t
