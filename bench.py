@@ -1,0 +1,315 @@
+"""Benchmark of the Gated DeltaNet hot path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+One step of the default workload is one pass of the whole hot path over one
+batch of synthetic input:
+  * gdn_decode on a batch of 64 sequences (32 value heads sharing 16 q/k heads,
+    d = 128, fp32 states [64, 32, 128, 128] updated in place), and
+  * gdn_prefill_varlen on 16 packed sequences with lengths uniform in
+    [128, 2048] (same heads, chunk 64, zero initial states).
+Inputs are resident in HBM before timing starts.  Decode cycles through four
+independent state buffers (4 x 128 MiB) so that successive steps cannot be
+served from the 256 MB last-level cache.
+
+The JSON line's ``value`` is the decode kernel's achieved HBM bandwidth
+(algorithmic bytes / kernel time, HIP events on the launch stream); the
+``prefill`` object carries tokens/s and MFMA utilisation.  ``roofline`` is the
+decode kernel against HBM peak; ``prefill.roofline`` the prefill launch against
+the bf16 MFMA peak.  Other workloads (``--workload``) print the same format.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, TFLOP/s
+METRIC = "decode: achieved HBM GB/s (% peak); prefill: tokens/s and MFMA util %"
+
+
+# --- algorithmic work ------------------------------------------------------------
+
+def decode_bytes(B, H_qk, H_v, D):
+    """State read + write (fp32), q/k (bf16, one read per q/k head), v and o
+    (bf16), g and beta (fp32)."""
+    return (2 * B * H_v * D * D * 4 + 2 * B * H_qk * D * 2 + 2 * B * H_v * D * 2
+            + 2 * B * H_v * 4)
+
+
+def prefill_flops(T, H_v, D, C):
+    """Dense chunked-form FLOPs per token: 2 H_v (4 C D + 3 D^2) (the C x C
+    products K K^T, Q K^T, T W, (M o QK^T) U and the D x D products K S^T,
+    Q S^T and the state update, each counted once, no hi/lo split)."""
+    return T * 2 * H_v * (4 * C * D + 3 * D * D)
+
+
+def prefill_bytes(T, N, H_qk, H_v, D, init_state):
+    per_tok = 2 * H_qk * D * 2 + 2 * H_v * D * 2 + 2 * H_v * 4
+    st = N * H_v * D * D * 4 * (2 if init_state else 1)
+    return T * per_tok + st
+
+
+# --- helpers ---------------------------------------------------------------------
+
+def _dev_inputs_decode(d, dev):
+    from paper_2607_17979_amd.workloads import to_torch
+
+    return dict(q=to_torch(d.q, dev, True), k=to_torch(d.k, dev, True), v=to_torch(d.v, dev, True),
+                g=to_torch(d.g, dev), beta=to_torch(d.beta, dev))
+
+
+def _dev_inputs_prefill(p, dev):
+    from paper_2607_17979_amd.workloads import to_torch
+
+    return dict(q=to_torch(p.q, dev, True), k=to_torch(p.k, dev, True), v=to_torch(p.v, dev, True),
+                g=to_torch(p.g, dev), beta=to_torch(p.beta, dev), cu=to_torch(p.cu_seqlens, dev),
+                init=to_torch(p.initial_state, dev))
+
+
+class Decode:
+    def __init__(self, dev, B, H_qk, H_v, D, seed, nbuf):
+        import torch
+        from paper_2607_17979_amd import workloads as wl
+
+        self.B, self.H_qk, self.H_v, self.D = B, H_qk, H_v, D
+        self.host = wl.decode_inputs(seed, B, H_qk, H_v, D)
+        self.x = _dev_inputs_decode(self.host, dev)
+        self.states = [wl.to_torch(self.host.state, dev) for _ in range(nbuf)]
+        self.o = torch.empty((B, H_v, D), dtype=torch.bfloat16, device=dev)
+        self.i = 0
+        self.bytes = decode_bytes(B, H_qk, H_v, D)
+
+    def __call__(self):
+        from paper_2607_17979_amd import gdn
+
+        x = self.x
+        gdn.gdn_decode(x["q"], x["k"], x["v"], x["g"], x["beta"], self.states[self.i % len(self.states)],
+                       self.o)
+        self.i += 1
+
+
+class Prefill:
+    def __init__(self, dev, lengths, H_qk, H_v, D, C, seed, state_std):
+        import torch
+        from paper_2607_17979_amd import gdn
+        from paper_2607_17979_amd import workloads as wl
+
+        self.host = wl.prefill_inputs(seed, lengths, H_qk, H_v, D, state_std=state_std)
+        self.x = _dev_inputs_prefill(self.host, dev)
+        N, T = len(lengths), int(sum(lengths))
+        self.N, self.T, self.H_qk, self.H_v, self.D, self.C = N, T, H_qk, H_v, D, C
+        self.fin = torch.empty((N, H_v, D, D), dtype=torch.float32, device=dev)
+        self.o = torch.empty((T, H_v, D), dtype=torch.bfloat16, device=dev)
+        ws = gdn.gdn_prefill_workspace_size(N, T, H_qk, H_v, D, D, C)
+        self.ws = torch.empty(max(ws, 256), dtype=torch.uint8, device=dev)
+        self.flops = prefill_flops(T, H_v, D, C)
+        self.bytes = prefill_bytes(T, N, H_qk, H_v, D, state_std is not None)
+
+    def __call__(self):
+        from paper_2607_17979_amd import gdn
+
+        x = self.x
+        gdn.gdn_prefill_varlen(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], x["init"],
+                               self.fin, self.o, chunk=self.C, workspace=self.ws)
+
+
+def _time_parts(parts, steps, warmup):
+    """Run ``warmup`` then ``steps`` steps of all parts in order; per-part HIP
+    event times on torch's current stream (the stream the library launches on)
+    and the wall time of the timed steps.  Returns (ms_per_step, [avg ms per part])."""
+    import torch
+
+    for _ in range(warmup):
+        for p in parts:
+            p()
+    torch.cuda.synchronize()
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in parts] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(steps):
+        for j, p in enumerate(parts):
+            evs[s][j][0].record()
+            p()
+            evs[s][j][1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = [sum(evs[s][j][0].elapsed_time(evs[s][j][1]) for s in range(steps)) / steps
+           for j in range(len(parts))]
+    return wall * 1e3 / steps, per
+
+
+def _cpu_baseline_decode(dec, budget_s=10.0):
+    """The fp64 oracle's decode (as it stands) timed on the host: repeated full
+    calls on the same batch until about ``budget_s`` of CPU time."""
+    import oracle.gdn_ref as ref
+
+    h = dec.host
+    n, t0 = 0, time.perf_counter()
+    while True:
+        ref.decode(h.q, h.k, h.v, h.g, h.beta, h.state)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    return dict(value=n * dec.bytes / el / 1e9, unit="GB/s", cores=1, kind="oracle",
+                sample=f"{n} full decode calls of the timed batch ({dec.B} x {dec.H_v} heads), "
+                       f"{el:.1f} s; numpy fp64 token loop, single-threaded einsum")
+
+
+def _cpu_baseline_prefill(pre, budget_s=10.0):
+    """The oracle's prefill on a bounded sample: whole (sequence, head) units of
+    the timed batch, one after another, until about ``budget_s``; scaled to
+    tokens/s of all heads (units are independent, so time is linear in units)."""
+    import oracle.gdn_ref as ref
+
+    h = pre.host
+    cu = h.cu_seqlens
+    unit_tokens, n_units, t0 = 0, 0, time.perf_counter()
+    while True:
+        seq = n_units % pre.N
+        head = (7 * n_units) % pre.H_v
+        ref.prefill_units(h.q, h.k, h.v, h.g, h.beta, cu, [(seq, head)], h.initial_state)
+        unit_tokens += int(cu[seq + 1] - cu[seq])
+        n_units += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    return dict(value=unit_tokens / pre.H_v / el, unit="tokens/s", cores=1, kind="oracle",
+                sample=f"{n_units} (sequence, head) units, {unit_tokens} unit-tokens, {el:.1f} s; "
+                       f"tokens/s = unit-tokens / H_v / seconds")
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="decode_b64+prefill_varlen16",
+                    choices=["decode_b64+prefill_varlen16", "decode_b64", "decode_sweep",
+                             "prefill_varlen16", "prefill_long2x64k"])
+    ap.add_argument("--batch", type=int, default=None, help="decode_sweep: one batch size only")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args(argv)
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the "
+              "per-GPU kernels shard by (sequence, head) with no exchange, see the design notes",
+              file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2607_17979_amd import workloads as wl
+    from paper_2607_17979_amd.build import LIB_PATH
+
+    if not os.path.exists(LIB_PATH):
+        from paper_2607_17979_amd.build import build
+
+        build()
+    dev = torch.device("cuda:0")
+    W = wl.WORKLOADS
+    out = dict(metric=METRIC, n_gpus=1, steps=args.steps, warmup=args.warmup,
+               higher_is_better=True, scaling="weak", vs_baseline=None, data="synthetic")
+    print(f"# bench {args.workload}: setting up inputs", file=sys.stderr, flush=True)
+
+    if args.workload in ("decode_b64+prefill_varlen16", "decode_b64", "decode_sweep"):
+        if args.workload == "decode_sweep":
+            w = W["decode_sweep"]
+            batches = [args.batch] if args.batch else list(w["batches"])
+        else:
+            w = W["decode_b64"]
+            batches = [w["B"]]
+    parts, names = [], []
+    dec = pre = None
+    if args.workload in ("decode_b64+prefill_varlen16", "decode_b64"):
+        w = W["decode_b64"]
+        dec = Decode(dev, w["B"], w["H_qk"], w["H_v"], w["D"], w["seed"], nbuf=4)
+        parts.append(dec)
+        names.append("decode")
+    if args.workload in ("decode_b64+prefill_varlen16", "prefill_varlen16"):
+        w = W["prefill_varlen16"]
+        lengths = wl.varlen_lengths(w["seed"], w["N"], w["len_lo"], w["len_hi"])
+        pre = Prefill(dev, lengths, w["H_qk"], w["H_v"], w["D"], w["chunk"], w["seed"], w["state_std"])
+        parts.append(pre)
+        names.append("prefill")
+    if args.workload == "prefill_long2x64k":
+        w = W["prefill_long2x64k"]
+        pre = Prefill(dev, [w["len"]] * w["N"], w["H_qk"], w["H_v"], w["D"], w["chunk"], w["seed"],
+                      w["state_std"])
+        parts.append(pre)
+        names.append("prefill")
+
+    if args.workload == "decode_sweep":
+        w = W["decode_sweep"]
+        lines = []
+        for B in batches:
+            nbuf = max(1, min(4, (512 << 20) // (B * w["H_v"] * w["D"] * w["D"] * 4)))
+            d = Decode(dev, B, w["H_qk"], w["H_v"], w["D"], w["seed"] + B, nbuf=nbuf)
+            ms_step, per = _time_parts([d], w["steps"], args.warmup)
+            gbs = d.bytes / (per[0] * 1e-3) / 1e9
+            lines.append(dict(batch=B, us_per_step=per[0] * 1e3, GBs=gbs, frac=gbs / HBM_PEAK_GBS,
+                              state_buffers=nbuf))
+            print(f"# decode B={B}: {per[0]*1e3:.2f} us/step, {gbs:.1f} GB/s", file=sys.stderr, flush=True)
+        big = lines[-1]
+        out.update(value=big["GBs"], unit="GB/s", ms_per_step=big["us_per_step"] / 1e3,
+                   steps=w["steps"], dtype="f32",
+                   config=dict(workload=f"decode sweep, batches {batches} x {w['steps']} steps, "
+                                        f"H_v={w['H_v']}/H_qk={w['H_qk']}, d={w['D']}",
+                               sweep=lines),
+                   roofline=dict(bound="hbm", achieved=big["GBs"], peak=HBM_PEAK_GBS, unit="GB/s",
+                                 frac=big["frac"], traffic=None))
+        print(json.dumps(out), flush=True)
+        return 0
+
+    print(f"# bench: timing {args.steps} steps after {args.warmup} warmup", file=sys.stderr, flush=True)
+    ms_step, per = _time_parts(parts, args.steps, args.warmup)
+    times = dict(zip(names, per))
+    out["ms_per_step"] = ms_step
+    cfg = {}
+    if dec is not None:
+        gbs = dec.bytes / (times["decode"] * 1e-3) / 1e9
+        out.update(value=gbs, unit="GB/s", dtype="f32")
+        out["roofline"] = dict(bound="hbm", achieved=gbs, peak=HBM_PEAK_GBS, unit="GB/s",
+                               frac=gbs / HBM_PEAK_GBS, traffic=None,
+                               kernel="gdn::decode_kernel<128,4>",
+                               bytes_per_launch=dec.bytes, us_per_launch=times["decode"] * 1e3)
+        cfg["decode"] = dict(B=dec.B, H_qk=dec.H_qk, H_v=dec.H_v, d=dec.D, state_buffers=len(dec.states))
+    if pre is not None:
+        t = times["prefill"] * 1e-3
+        tflops = pre.flops / t / 1e12
+        pobj = dict(tokens_per_s=pre.T / t, us_per_call=t * 1e6, tokens=pre.T, sequences=pre.N,
+                    algorithmic_tflops=tflops, mfma_util=tflops / BF16_PEAK_TFLOPS,
+                    hbm_GBs=pre.bytes / t / 1e9,
+                    roofline=dict(bound="mfma", achieved=tflops, peak=BF16_PEAK_TFLOPS,
+                                  unit="TFLOP/s", frac=tflops / BF16_PEAK_TFLOPS, traffic=None,
+                                  kernel="gdn::prefill_kernel<128,64> (+ schedule kernel)",
+                                  flops_per_launch=pre.flops))
+        out["prefill"] = pobj
+        cfg["prefill"] = dict(N=pre.N, T=pre.T, H_qk=pre.H_qk, H_v=pre.H_v, d=pre.D, chunk=pre.C,
+                              initial_state=pre.host.initial_state is not None)
+        if dec is None:
+            out.update(value=pre.T / t, unit="tokens/s", dtype="bf16-mfma/f32")
+            out["roofline"] = pobj["roofline"]
+    out["config"] = dict(workload=args.workload, **cfg)
+    if not args.no_cpu_baseline:
+        print("# bench: timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
+        if dec is not None:
+            out["cpu_baseline"] = _cpu_baseline_decode(dec)
+            if pre is not None:
+                out["prefill"]["cpu_baseline"] = _cpu_baseline_prefill(pre)
+        else:
+            out["cpu_baseline"] = _cpu_baseline_prefill(pre)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

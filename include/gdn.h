@@ -1,0 +1,140 @@
+/*
+ * gdn.h -- C ABI of the MI355X (gfx950) Gated DeltaNet library.
+ *
+ * The operation (paper: appendix "Operator Background and Mathematical
+ * Definitions", subsection "Gated Delta Net", the gated delta rule), per
+ * sequence and value head, token by token:
+ *
+ *     S_t = S_{t-1} ( alpha_t (I - beta_t k_t k_t^T) ) + beta_t v_t k_t^T
+ *     o_t = scale * S_t q_t,          alpha_t = exp(g_t)
+ *
+ * in the two execution regimes the same subsection names: decode (one new
+ * token per sequence on a prior state) and prefill (whole packed sequences,
+ * returning every output and the final state).
+ *
+ * Conventions shared by every entry point:
+ *   - Pointers are DEVICE pointers unless stated otherwise.  Tensors are dense
+ *     and row-major (last index contiguous).  bf16 tensors are passed as
+ *     untyped pointers to 2-byte IEEE bfloat16 values.
+ *   - The state S of one (sequence, value head) is d_v x d_k fp32, stored with
+ *     the k index contiguous: state[..., i, j] = S[i][j], i < d_v, j < d_k.
+ *   - Value head h reads q/k head floor(h * H_qk / H_v) (H_v must be a multiple
+ *     of H_qk; consecutive value heads share a q/k head).
+ *   - g is the natural-log gate (alpha = exp(g), normally g <= 0); beta is the
+ *     write strength, one fp32 scalar per (token, value head).
+ *   - o is written as bf16, rounded to nearest even from fp32.
+ *   - Ownership: the caller owns every buffer; the library allocates, frees
+ *     and synchronises nothing.  Calls are asynchronous on `stream`
+ *     (a hipStream_t; NULL = the null stream).
+ *   - Supported shapes: d_k == d_v == D with D in {16, 128}; prefill chunk
+ *     C = 16 for D = 16 and C = 64 for D = 128.
+ *   - Alignment: q, k, v, o and state pointers must be 16-byte aligned;
+ *     g, beta and cu_seqlens 4-byte aligned.
+ *   - Errors: every argument check runs on the host before any HIP call.  A
+ *     failed check returns a negative gdn_status, records a message for
+ *     gdn_last_error() and launches nothing.  A failed launch returns GDN_EHIP.
+ *     Faults inside a kernel surface at the caller's next synchronisation.
+ *   - Not re-entrant on overlapping outputs: two calls in flight that write the
+ *     same state or output memory race.
+ */
+#ifndef GDN_MI355X_H
+#define GDN_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__)
+#define GDN_API __attribute__((visibility("default")))
+#else
+#define GDN_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum gdn_status {
+    GDN_OK = 0,
+    GDN_EINVAL = -1,       /* null pointer, negative size, bad head ratio, bad cu_seqlens */
+    GDN_EUNSUPPORTED = -2, /* head dim or chunk size outside the supported set */
+    GDN_EALIGN = -3,       /* pointer not aligned as required */
+    GDN_EWORKSPACE = -4,   /* workspace missing or smaller than required */
+    GDN_EHIP = -5          /* a HIP runtime call or kernel launch failed */
+} gdn_status;
+
+/* Message for the most recent non-OK status returned on the calling host
+ * thread ("" if none).  The pointer stays valid until the next library call
+ * on that thread. */
+GDN_API const char* gdn_last_error(void);
+
+/* Library ABI version (major * 100 + minor). */
+GDN_API int gdn_abi_version(void);
+
+/*
+ * gdn_decode -- one recurrent step for B sequences (the decode regime).
+ *
+ *   q, k   bf16 [B, H_qk, D]
+ *   v      bf16 [B, H_v, D]
+ *   g      fp32 [B, H_v]            log gate, alpha = exp(g)
+ *   beta   fp32 [B, H_v]
+ *   state  fp32 [B, H_v, D, D]      read, then overwritten IN PLACE with S_t
+ *   o      bf16 [B, H_v, D]         o = scale * S_t q  (post-update state)
+ *
+ * Each state is streamed through HBM once.  B = 0 is a no-op returning GDN_OK
+ * (pointers are then not checked).  `o` must not overlap any input.
+ */
+GDN_API int gdn_decode(const void* q, const void* k, const void* v,
+               const float* g, const float* beta,
+               float* state, void* o,
+               int B, int H_qk, int H_v, int D_k, int D_v,
+               float scale, void* stream);
+
+/*
+ * Bytes of device workspace gdn_prefill_varlen needs for N sequences (the
+ * longest-first schedule: one int32 per sequence, rounded up to 256 bytes).
+ * Returns 0 for invalid arguments.
+ */
+GDN_API size_t gdn_prefill_workspace_size(int N, int T, int H_qk, int H_v,
+                                  int D_k, int D_v, int chunk);
+
+/*
+ * gdn_prefill_varlen -- packed variable-length prefill (the prefill regime),
+ * computed in chunks of `chunk` tokens aligned to each sequence's first token
+ * (the last chunk of a sequence may be shorter); the result equals the
+ * token-by-token recurrence up to rounding.
+ *
+ *   q, k           bf16 [T, H_qk, D]
+ *   v              bf16 [T, H_v, D]
+ *   g, beta        fp32 [T, H_v]
+ *   cu_seqlens     int32 [N + 1], device: sequence n is tokens
+ *                  [cu_seqlens[n], cu_seqlens[n+1]).  Must hold cu[0] = 0,
+ *                  non-decreasing, cu[N] = T.  The library never reads it on
+ *                  the host and trusts it: a violation is undefined behaviour
+ *                  (out-of-bounds device reads included).  Zero-length
+ *                  sequences are allowed: their final state is their initial
+ *                  state.
+ *   initial_state  fp32 [N, H_v, D, D] or NULL (zero state)
+ *   final_state    fp32 [N, H_v, D, D]; may be the same pointer as
+ *                  initial_state (in-place), must not partially overlap it.
+ *   o              bf16 [T, H_v, D]
+ *   workspace      device buffer of at least
+ *                  gdn_prefill_workspace_size(...) bytes, 256-byte aligned;
+ *                  its contents are scratch (overwritten by each call).
+ *
+ * N = 0 is a no-op returning GDN_OK.
+ */
+GDN_API int gdn_prefill_varlen(const void* q, const void* k, const void* v,
+                       const float* g, const float* beta,
+                       const int32_t* cu_seqlens,
+                       const float* initial_state, float* final_state,
+                       void* o,
+                       int N, int T, int H_qk, int H_v, int D_k, int D_v,
+                       int chunk, float scale,
+                       void* workspace, size_t workspace_bytes,
+                       void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GDN_MI355X_H */

@@ -1,0 +1,132 @@
+// C ABI entry points: host-side argument checks, then the kernel launchers.
+// No check touches the HIP runtime, so every error path can be exercised on a
+// machine without a GPU.
+#include "../../include/gdn.h"
+
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "gdn_launch.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return status;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int check_heads(int H_qk, int H_v, int D_k, int D_v) {
+    if (H_qk <= 0 || H_v <= 0)
+        return fail(GDN_EINVAL, "head counts must be positive (H_qk=%d, H_v=%d)", H_qk, H_v);
+    if (H_v % H_qk != 0)
+        return fail(GDN_EINVAL, "H_v (%d) must be a multiple of H_qk (%d)", H_v, H_qk);
+    if (D_k != D_v)
+        return fail(GDN_EUNSUPPORTED, "d_k (%d) must equal d_v (%d)", D_k, D_v);
+    if (D_k != 16 && D_k != 128)
+        return fail(GDN_EUNSUPPORTED, "head dim %d unsupported (supported: 16, 128)", D_k);
+    return GDN_OK;
+}
+
+int check_ptr16(const void* p, const char* name) {
+    if (p == nullptr) return fail(GDN_EINVAL, "%s is NULL", name);
+    if (!aligned(p, 16)) return fail(GDN_EALIGN, "%s is not 16-byte aligned", name);
+    return GDN_OK;
+}
+
+int check_ptr4(const void* p, const char* name) {
+    if (p == nullptr) return fail(GDN_EINVAL, "%s is NULL", name);
+    if (!aligned(p, 4)) return fail(GDN_EALIGN, "%s is not 4-byte aligned", name);
+    return GDN_OK;
+}
+
+int chunk_for(int D) { return D == 16 ? 16 : 64; }
+
+}  // namespace
+
+extern "C" {
+
+const char* gdn_last_error(void) { return g_last_error.c_str(); }
+
+int gdn_abi_version(void) { return 100; }
+
+int gdn_decode(const void* q, const void* k, const void* v, const float* g, const float* beta,
+               float* state, void* o, int B, int H_qk, int H_v, int D_k, int D_v, float scale,
+               void* stream) {
+    g_last_error.clear();
+    if (B < 0) return fail(GDN_EINVAL, "B must be >= 0 (got %d)", B);
+    if (int st = check_heads(H_qk, H_v, D_k, D_v)) return st;
+    if (B == 0) return GDN_OK;
+    if ((long long)B * H_v > (1LL << 30))
+        return fail(GDN_EINVAL, "B * H_v = %lld too large", (long long)B * H_v);
+    int st;
+    if ((st = check_ptr16(q, "q")) || (st = check_ptr16(k, "k")) || (st = check_ptr16(v, "v")) ||
+        (st = check_ptr16(state, "state")) || (st = check_ptr16(o, "o")) ||
+        (st = check_ptr4(g, "g")) || (st = check_ptr4(beta, "beta")))
+        return st;
+    gdn::DecodeArgs a{q, k, v, g, beta, state, o, B, H_qk, H_v, D_k, scale};
+    hipError_t e = gdn::launch_decode(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(GDN_EHIP, "decode launch failed: %s", hipGetErrorString(e));
+    return GDN_OK;
+}
+
+size_t gdn_prefill_workspace_size(int N, int T, int H_qk, int H_v, int D_k, int D_v, int chunk) {
+    if (N < 0 || T < 0 || H_qk <= 0 || H_v <= 0 || H_v % H_qk || D_k != D_v ||
+        (D_k != 16 && D_k != 128) || chunk != chunk_for(D_k))
+        return 0;
+    return gdn::prefill_workspace_bytes(N);
+}
+
+int gdn_prefill_varlen(const void* q, const void* k, const void* v, const float* g,
+                       const float* beta, const int32_t* cu_seqlens, const float* initial_state,
+                       float* final_state, void* o, int N, int T, int H_qk, int H_v, int D_k,
+                       int D_v, int chunk, float scale, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+    g_last_error.clear();
+    if (N < 0 || T < 0) return fail(GDN_EINVAL, "N and T must be >= 0 (N=%d, T=%d)", N, T);
+    if (int st = check_heads(H_qk, H_v, D_k, D_v)) return st;
+    if (chunk != chunk_for(D_k))
+        return fail(GDN_EUNSUPPORTED, "chunk %d unsupported for head dim %d (use %d)", chunk, D_k,
+                    chunk_for(D_k));
+    if (N == 0) return GDN_OK;
+    if ((long long)T * H_v > (1LL << 31) / 128 || (long long)N * H_v > (1LL << 30))
+        return fail(GDN_EINVAL, "problem too large (N=%d, T=%d, H_v=%d)", N, T, H_v);
+    int st;
+    if ((st = check_ptr4(cu_seqlens, "cu_seqlens")) || (st = check_ptr16(final_state, "final_state")))
+        return st;
+    if (initial_state != nullptr && !aligned(initial_state, 16))
+        return fail(GDN_EALIGN, "initial_state is not 16-byte aligned");
+    if (initial_state != nullptr && initial_state != final_state) {
+        const char* a0 = reinterpret_cast<const char*>(initial_state);
+        const char* b0 = reinterpret_cast<const char*>(final_state);
+        const size_t bytes = (size_t)N * H_v * D_k * D_k * sizeof(float);
+        if (a0 < b0 + bytes && b0 < a0 + bytes)
+            return fail(GDN_EINVAL, "initial_state and final_state overlap without being equal");
+    }
+    if (T > 0) {
+        if ((st = check_ptr16(q, "q")) || (st = check_ptr16(k, "k")) || (st = check_ptr16(v, "v")) ||
+            (st = check_ptr16(o, "o")) || (st = check_ptr4(g, "g")) || (st = check_ptr4(beta, "beta")))
+            return st;
+    }
+    const size_t need = gdn::prefill_workspace_bytes(N);
+    if (workspace == nullptr || workspace_bytes < need)
+        return fail(GDN_EWORKSPACE, "workspace of %zu bytes needed, %zu given%s", need,
+                    workspace_bytes, workspace == nullptr ? " (NULL)" : "");
+    if (!aligned(workspace, 256)) return fail(GDN_EALIGN, "workspace is not 256-byte aligned");
+    gdn::PrefillArgs a{q, k, v, g, beta, cu_seqlens, initial_state, final_state, o,
+                       N, T, H_qk, H_v, D_k, chunk, scale, workspace};
+    hipError_t e = gdn::launch_prefill(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(GDN_EHIP, "prefill launch failed: %s", hipGetErrorString(e));
+    return GDN_OK;
+}
+
+}  // extern "C"

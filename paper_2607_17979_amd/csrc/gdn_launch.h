@@ -1,0 +1,45 @@
+// Host-side launch interface between the C ABI layer (argument checks) and
+// the kernel files.  Arguments reaching these functions are already checked.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace gdn {
+
+struct DecodeArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    const float* g;
+    const float* beta;
+    float* state;
+    void* o;
+    int B, H_qk, H_v, D;
+    float scale;
+};
+
+struct PrefillArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    const float* g;
+    const float* beta;
+    const int32_t* cu_seqlens;
+    const float* initial_state;
+    float* final_state;
+    void* o;
+    int N, T, H_qk, H_v, D, chunk;
+    float scale;
+    void* workspace;
+};
+
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
+hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream);
+
+// Workspace layout of the prefill: int32 order[N] (sequence indices sorted by
+// length, longest first, ties by index), rounded up to 256 bytes.
+size_t prefill_workspace_bytes(int N);
+
+}  // namespace gdn

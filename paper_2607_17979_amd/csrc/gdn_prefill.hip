@@ -1,0 +1,591 @@
+// Prefill regime of the gated delta rule (paper: appendix "Operator Background
+// and Mathematical Definitions", subsection "Gated Delta Net": the whole
+// sequence is evaluated and both outputs and the final state are returned, by
+// chunked matrix operations that apply the log-domain gate consistently).
+//
+// Chunked form used here (an exact regrouping of the token recurrence).  For a
+// chunk of rows r = 0..C-1 of one (sequence, value head), gamma_r = running sum
+// of g inside the chunk, S0 = state entering the chunk (d_v x d_k):
+//     A_ri = beta_r exp(gamma_r - gamma_i) (k_r . k_i)   (i < r, else 0)
+//     T    = (I + A)^-1                                  (unit lower triangular)
+//     W    = V - diag(exp(gamma)) K S0^T
+//     U    = T diag(beta) W
+//     O    = scale (diag(exp(gamma)) Q S0^T + (M o Q K^T) U),
+//            M_ri = exp(gamma_r - gamma_i) for i <= r, else 0
+//     S    = exp(gamma_{C-1}) S0 + (diag(exp(gamma_{C-1} - gamma)) U)^T K
+// Chunks start at each sequence's first token; the ragged last chunk is padded
+// with q = k = v = 0, g = 0, beta = 0 rows, which contribute exactly nothing.
+//
+// Work decomposition (gfx950, one workgroup per (sequence, value head)):
+//   * NW waves; wave w owns value columns [w VW, (w+1) VW) of the state, held
+//     transposed (S^T, d x v) in fp32 MFMA accumulators across all chunks.
+//   * Per chunk: stage Q, K, V rows in LDS (row-major bf16) and K^T; the gate
+//     prefix sum; the lower-triangular tiles of K K^T and Q K^T on bf16 MFMA
+//     (exact bf16 operands); masks and decays in fp32; T by 16 x 16 diagonal
+//     forward substitution plus fp32-MFMA block levels; T diag(beta) stored as
+//     a bf16 hi + lo pair.
+//   * State-dependent part per wave on bf16 MFMA with fp32 accumulation.
+//     Operands that are computed fp32 values feeding the state are split into
+//     hi + lo bf16 (x = hi + lo to ~2^-17): S0 in K S0^T, W and T diag(beta)
+//     in U (hi*hi + hi*lo + lo*hi), and U in the state update.  The output-only
+//     products (Q S0^T, (M o QK^T) U) use the hi parts.
+//   * Accumulator tiles feed the next MFMA directly as B operands: for a
+//     32-deep contraction slice, lane group g holds accumulator rows 4g..4g+3
+//     of two 16-row tiles, and the matching A operand is read from LDS in the
+//     same permuted contraction order (two 8-byte reads per lane).
+#include "gdn_device.h"
+#include "gdn_launch.h"
+
+namespace gdn {
+
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+
+// --- MFMA wrappers -----------------------------------------------------------
+// K = 32: v_mfma_f32_16x16x32_bf16 (gfx950); K = 16: v_mfma_f32_16x16x16_bf16.
+// Layout (both): A[m][k] on lane m + 16 g, B[k][n] on lane n + 16 g, slot j of
+// the lane's operand vector is contraction index (K/4) g + j in hardware order;
+// D[4 g + i][n] on lane n + 16 g, element i.  Only the pairing of A and B
+// slots matters for a contraction, so operands may use any common order.
+template <int K> struct Frag;
+template <> struct Frag<32> { typedef bf16x8_t type; };
+template <> struct Frag<16> { typedef s16x4_t type; };
+
+__device__ __forceinline__ f32x4_t mma(const bf16x8_t& a, const bf16x8_t& b, const f32x4_t& c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4_t mma(const s16x4_t& a, const s16x4_t& b, const f32x4_t& c) {
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+
+// fp32 MFMA 16x16x4: A[m][k] on lane m + 16 k, B[k][n] on lane n + 16 k.
+__device__ __forceinline__ f32x4_t mma_f32(float a, float b, const f32x4_t& c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// A/B operand from a row-major bf16 LDS matrix, "permuted" contraction order:
+// slot j < 4 -> column k0 + 4g + j, slot j >= 4 -> k0 + 16 + 4g + (j - 4).
+// This is the order in which accumulator tiles supply B operands.
+template <int K>
+__device__ __forceinline__ typename Frag<K>::type lds_frag_perm(const uint16_t* row, int k0, int g) {
+    if constexpr (K == 32) {
+        const uint2 lo = *reinterpret_cast<const uint2*>(row + k0 + 4 * g);
+        const uint2 hi = *reinterpret_cast<const uint2*>(row + k0 + 16 + 4 * g);
+        uint4 u = {lo.x, lo.y, hi.x, hi.y};
+        return __builtin_bit_cast(bf16x8_t, u);
+    } else {
+        const uint2 u = *reinterpret_cast<const uint2*>(row + k0 + 4 * g);
+        return __builtin_bit_cast(s16x4_t, u);
+    }
+}
+
+// Operand in "natural" order (slot j -> column k0 + (K/4) g + j); used where
+// both operands come from LDS.
+template <int K>
+__device__ __forceinline__ typename Frag<K>::type lds_frag_nat(const uint16_t* row, int k0, int g) {
+    if constexpr (K == 32) {
+        const uint4 u = *reinterpret_cast<const uint4*>(row + k0 + 8 * g);
+        return __builtin_bit_cast(bf16x8_t, u);
+    } else {
+        const uint2 u = *reinterpret_cast<const uint2*>(row + k0 + 4 * g);
+        return __builtin_bit_cast(s16x4_t, u);
+    }
+}
+
+__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
+    return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+}
+
+// Round x to bf16 hi and the residual x - hi to bf16 lo.
+__device__ __forceinline__ void split_bf16(float x, float& hi, float& lo) {
+    hi = bf16_to_f32(f32_to_bf16(x));
+    lo = x - hi;
+}
+
+// B operand from accumulator tiles t0 (contraction rows k0..k0+15) and t1
+// (rows k0+16..k0+31), hi part and lo residual, in the permuted order.
+template <int K>
+__device__ __forceinline__ void acc_frag(const f32x4_t& t0, const f32x4_t& t1, float mul0[4],
+                                         float mul1[4], typename Frag<K>::type& hi,
+                                         typename Frag<K>::type& lo) {
+    float h[8], l[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) split_bf16(t0[i] * mul0[i], h[i], l[i]);
+    if constexpr (K == 32) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) split_bf16(t1[i] * mul1[i], h[4 + i], l[4 + i]);
+        uint4 uh = {pack_bf16(h[0], h[1]), pack_bf16(h[2], h[3]), pack_bf16(h[4], h[5]),
+                    pack_bf16(h[6], h[7])};
+        uint4 ul = {pack_bf16(l[0], l[1]), pack_bf16(l[2], l[3]), pack_bf16(l[4], l[5]),
+                    pack_bf16(l[6], l[7])};
+        hi = __builtin_bit_cast(bf16x8_t, uh);
+        lo = __builtin_bit_cast(bf16x8_t, ul);
+    } else {
+        uint2 uh = {pack_bf16(h[0], h[1]), pack_bf16(h[2], h[3])};
+        uint2 ul = {pack_bf16(l[0], l[1]), pack_bf16(l[2], l[3])};
+        hi = __builtin_bit_cast(s16x4_t, uh);
+        lo = __builtin_bit_cast(s16x4_t, ul);
+    }
+}
+
+// --- configuration -------------------------------------------------------------
+template <int D, int C>
+struct Cfg {
+    static constexpr int NW = (D == 128) ? 4 : 1;  // waves per workgroup
+    static constexpr int NT = 64 * NW;             // threads
+    static constexpr int VW = D / NW;              // value columns per wave (32 or 16)
+    static constexpr int NVT = VW / 16;            // 16-wide value tiles per wave
+    static constexpr int NDT = D / 16;             // 16-row d tiles
+    static constexpr int NCT = C / 16;             // 16-row chunk tiles
+    static constexpr int KD = D >= 32 ? 32 : 16;   // contraction step over d
+    static constexpr int KC = C >= 32 ? 32 : 16;   // contraction step over chunk rows
+    static constexpr int PD = D + 8;               // LDS pitch (bf16) of [C][D] arrays
+    static constexpr int PC = C + 8;               // LDS pitch (bf16) of [.][C] arrays
+    static constexpr int PF = C + 4;               // LDS pitch (fp32) of [C][C] arrays
+    static_assert(NW == NCT, "one wave per diagonal 16x16 block of T");
+};
+
+template <int D, int C>
+struct Smem {
+    typedef Cfg<D, C> P;
+    uint16_t q[C][P::PD];
+    uint16_t k[C][P::PD];
+    uint16_t v[C][P::PD];
+    uint16_t kt[D][P::PC];   // K^T
+    uint16_t th[C][P::PC];   // T diag(beta), bf16 hi
+    uint16_t tl[C][P::PC];   // T diag(beta), bf16 lo
+    uint16_t pm[C][P::PC];   // (M o Q K^T), bf16
+    union {
+        struct {
+            float a[C][P::PF];  // A (strictly lower)
+            float t[C][P::PF];  // T (lower, unit diagonal)
+        } f;
+        uint16_t o[C][P::PD];   // output staging
+    } u;
+    float gam[C];   // gamma (running sum of g)
+    float eg[C];    // exp(gamma)
+    float egl[C];   // exp(gamma_last - gamma)
+    float beta[C];
+    float graw[C];
+};
+
+// --- schedule: sequences by length, longest first (ties by index) ---------------
+constexpr int kSortMax = 4096;
+
+__global__ __launch_bounds__(256) void prefill_schedule_kernel(const int32_t* __restrict__ cu,
+                                                               int N, int32_t* __restrict__ order) {
+    __shared__ int len[kSortMax];
+    if (N > kSortMax) {
+        for (int i = threadIdx.x; i < N; i += blockDim.x) order[i] = i;
+        return;
+    }
+    for (int i = threadIdx.x; i < N; i += blockDim.x) len[i] = cu[i + 1] - cu[i];
+    __syncthreads();
+    for (int i = threadIdx.x; i < N; i += blockDim.x) {
+        const int li = len[i];
+        int rank = 0;
+        for (int j = 0; j < N; ++j) {
+            const int lj = len[j];
+            rank += (lj > li) || (lj == li && j < i);
+        }
+        order[rank] = i;
+    }
+}
+
+// blockIdx -> logical work index.  Work items 2j and 2j+1 (two value heads
+// sharing a q/k head, same sequence) go to workgroups 8 apart, which the
+// dispatcher places on the same XCD, so their q/k reads share that L2.
+__device__ __forceinline__ int logical_item(int bid, int total) {
+    const int grp = bid >> 4;
+    if ((grp << 4) + 16 > total) return bid;
+    const int r = bid & 15;
+    return (grp << 4) + 2 * (r & 7) + (r >> 3);
+}
+
+// --- the chunk kernel ----------------------------------------------------------
+template <int D, int C>
+__global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+    const uint16_t* __restrict__ v, const float* __restrict__ g,
+    const float* __restrict__ beta, const int32_t* __restrict__ cu,
+    const int32_t* __restrict__ order, const float* initial_state, float* final_state,
+    uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale) {
+    typedef Cfg<D, C> P;
+    constexpr int KD = P::KD, KC = P::KC;
+    typedef typename Frag<KD>::type FD;
+    typedef typename Frag<KC>::type FC;
+    __shared__ Smem<D, C> sm;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int m = lane & 15;  // row / column within a 16x16 tile
+    const int gq = lane >> 4; // lane group (0..3)
+
+    const int item = logical_item(blockIdx.x, N * H_v);
+    const int rank = item / H_v;
+    const int h = item - rank * H_v;
+    const int n = order[rank];
+    const int hq = h / (H_v / H_qk);
+    const int seq_beg = cu[n];
+    const int seq_len = cu[n + 1] - seq_beg;
+    const int vcol0 = wave * P::VW;
+
+    // State S^T (d x v) for this wave's value columns, fp32 accumulators:
+    // st[dt][vt][i] = S[v][d], v = vcol0 + 16 vt + m, d = 16 dt + 4 gq + i.
+    f32x4_t st[P::NDT][P::NVT];
+    const size_t state_off = ((size_t)n * H_v + h) * D * D;
+#pragma unroll
+    for (int dt = 0; dt < P::NDT; ++dt)
+#pragma unroll
+        for (int vt = 0; vt < P::NVT; ++vt) {
+            if (initial_state != nullptr) {
+                const float4 s4 = *reinterpret_cast<const float4*>(
+                    initial_state + state_off + (size_t)(vcol0 + 16 * vt + m) * D + 16 * dt + 4 * gq);
+                st[dt][vt] = f32x4_t{s4.x, s4.y, s4.z, s4.w};
+            } else {
+                st[dt][vt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            }
+        }
+
+    // Blocks strictly above the diagonal of T diag(beta) and of the masked
+    // scores stay zero for the whole kernel; the diagonal blocks are rewritten
+    // (upper part included) every chunk.
+    for (int i = tid; i < C * C; i += P::NT) {
+        const int r = i / C, cc = i - r * C;
+        if ((cc >> 4) > (r >> 4)) { sm.th[r][cc] = 0; sm.tl[r][cc] = 0; sm.pm[r][cc] = 0; }
+    }
+
+    const size_t qk_stride = (size_t)H_qk * D;
+    const size_t v_stride = (size_t)H_v * D;
+
+    for (int c0 = 0; c0 < seq_len; c0 += C) {
+        const int L = min(C, seq_len - c0);
+        const int t0 = seq_beg + c0;
+
+        // ---- stage the chunk ---------------------------------------------------
+        // (the previous iteration ended with a barrier; the output staging of the
+        // previous chunk lives in sm.u and is flushed below before sm.u is reused)
+        for (int i = tid; i < C * (D / 8); i += P::NT) {
+            const int r = i / (D / 8), seg = i - r * (D / 8);
+            uint4 qv = {0, 0, 0, 0}, kv = {0, 0, 0, 0}, vv = {0, 0, 0, 0};
+            if (r < L) {
+                const size_t tq = (size_t)(t0 + r) * qk_stride + (size_t)hq * D + seg * 8;
+                qv = *reinterpret_cast<const uint4*>(q + tq);
+                kv = *reinterpret_cast<const uint4*>(k + tq);
+                vv = *reinterpret_cast<const uint4*>(v + (size_t)(t0 + r) * v_stride + (size_t)h * D + seg * 8);
+            }
+            *reinterpret_cast<uint4*>(&sm.q[r][seg * 8]) = qv;
+            *reinterpret_cast<uint4*>(&sm.k[r][seg * 8]) = kv;
+            *reinterpret_cast<uint4*>(&sm.v[r][seg * 8]) = vv;
+        }
+        for (int i = tid; i < C; i += P::NT) {
+            const bool in = i < L;
+            sm.graw[i] = in ? g[(size_t)(t0 + i) * H_v + h] : 0.f;
+            sm.beta[i] = in ? beta[(size_t)(t0 + i) * H_v + h] : 0.f;
+        }
+        __syncthreads();
+
+        // ---- gate prefix, K^T, raw score tiles -----------------------------------
+        if (wave == 0) {
+            float x = lane < C ? sm.graw[lane] : 0.f;
+#pragma unroll
+            for (int d = 1; d < 64; d <<= 1) {
+                const float y = __shfl_up(x, d);
+                if (lane >= d) x += y;
+            }
+            const float last = __shfl(x, C - 1);
+            if (lane < C) {
+                sm.gam[lane] = x;
+                sm.eg[lane] = fast_exp(x);
+                sm.egl[lane] = fast_exp(last - x);
+            }
+        }
+        for (int i = tid; i < (C / 2) * (D / 8); i += P::NT) {
+            const int p = i % (C / 2), seg = i / (C / 2);
+            const uint4 r0 = *reinterpret_cast<const uint4*>(&sm.k[2 * p][seg * 8]);
+            const uint4 r1 = *reinterpret_cast<const uint4*>(&sm.k[2 * p + 1][seg * 8]);
+            const uint32_t a[4] = {r0.x, r0.y, r0.z, r0.w};
+            const uint32_t b[4] = {r1.x, r1.y, r1.z, r1.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                *reinterpret_cast<uint32_t*>(&sm.kt[seg * 8 + 2 * j][2 * p]) =
+                    (a[j] & 0xFFFFu) | (b[j] << 16);
+                *reinterpret_cast<uint32_t*>(&sm.kt[seg * 8 + 2 * j + 1][2 * p]) =
+                    (a[j] >> 16) | (b[j] & 0xFFFF0000u);
+            }
+        }
+        // lower-triangular 16x16 tiles of G = K K^T (job < NTRI) and P = Q K^T
+        constexpr int NTRI = P::NCT * (P::NCT + 1) / 2;
+        constexpr int NJOB = 2 * NTRI;
+        constexpr int JPW = (NJOB + P::NW - 1) / P::NW;
+        f32x4_t gp[JPW];
+#pragma unroll
+        for (int jj = 0; jj < JPW; ++jj) {
+            gp[jj] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            const int job = wave + jj * P::NW;
+            if (job < NJOB) {
+                const int tri = job % NTRI;
+                int ti = 0;
+                while ((ti + 1) * (ti + 2) / 2 <= tri) ++ti;
+                const int tj = tri - ti * (ti + 1) / 2;
+                const uint16_t* arow = (job < NTRI ? &sm.k[0][0] : &sm.q[0][0]) + (16 * ti + m) * P::PD;
+                const uint16_t* brow = &sm.k[16 * tj + m][0];
+#pragma unroll
+                for (int kk = 0; kk < D; kk += KD)
+                    gp[jj] = mma(lds_frag_nat<KD>(arow, kk, gq), lds_frag_nat<KD>(brow, kk, gq), gp[jj]);
+            }
+        }
+        __syncthreads();
+
+        // ---- masks and decays: A (fp32) and M o Q K^T (bf16) ----------------------
+#pragma unroll
+        for (int jj = 0; jj < JPW; ++jj) {
+            const int job = wave + jj * P::NW;
+            if (job < NJOB) {
+                const int tri = job % NTRI;
+                int ti = 0;
+                while ((ti + 1) * (ti + 2) / 2 <= tri) ++ti;
+                const int tj = tri - ti * (ti + 1) / 2;
+                const int col = 16 * tj + m;
+                const float gcol = sm.gam[col];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int row = 16 * ti + 4 * gq + i;
+                    const float dec = fast_exp(sm.gam[row] - gcol);
+                    if (job < NTRI) {
+                        sm.u.f.a[row][col] = col < row ? sm.beta[row] * dec * gp[jj][i] : 0.f;
+                    } else {
+                        sm.pm[row][col] = f32_to_bf16(col <= row ? dec * gp[jj][i] : 0.f);
+                    }
+                }
+            }
+        }
+        __syncthreads();
+
+        // ---- T = (I + A)^-1 -------------------------------------------------------
+        // diagonal blocks by forward substitution: wave w, lane j < 16 -> column j
+        // of block w.
+        {
+            const int b = wave;
+            float x[16];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                float acc = (r == m) ? 1.f : 0.f;
+#pragma unroll
+                for (int i = 0; i < r; ++i) acc = fmaf(-sm.u.f.a[16 * b + r][16 * b + i], x[i], acc);
+                x[r] = acc;
+            }
+            if (lane < 16) {
+                const float bcol = sm.beta[16 * b + m];
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    sm.u.f.t[16 * b + r][16 * b + m] = x[r];
+                    float hi, lo;
+                    split_bf16(x[r] * bcol, hi, lo);
+                    sm.th[16 * b + r][16 * b + m] = f32_to_bf16(hi);
+                    sm.tl[16 * b + r][16 * b + m] = f32_to_bf16(lo);
+                }
+            }
+        }
+        __syncthreads();
+        // off-diagonal blocks, level by level: T_bj = -T_bb sum_{k=j}^{b-1} A_bk T_kj
+#pragma unroll
+        for (int lev = 1; lev < P::NCT; ++lev) {
+            const int j = wave;
+            const int b = j + lev;
+            if (b < P::NCT) {
+                f32x4_t y = {0.f, 0.f, 0.f, 0.f};
+                for (int kb = j; kb < b; ++kb) {
+#pragma unroll
+                    for (int s = 0; s < 4; ++s)
+                        y = mma_f32(sm.u.f.a[16 * b + m][16 * kb + 4 * s + gq],
+                                    sm.u.f.t[16 * kb + 4 * s + gq][16 * j + m], y);
+                }
+                // y is an accumulator: lane (n = m, group gq) holds Y[4 gq + i][n].  As
+                // the B operand of step s it supplies contraction row 4 gq + s.
+                f32x4_t z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int s = 0; s < 4; ++s)
+                    z = mma_f32(-sm.u.f.t[16 * b + m][16 * b + 4 * gq + s], y[s], z);
+                const float bcol = sm.beta[16 * j + m];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int row = 16 * b + 4 * gq + i;
+                    sm.u.f.t[row][16 * j + m] = z[i];
+                    float hi, lo;
+                    split_bf16(z[i] * bcol, hi, lo);
+                    sm.th[row][16 * j + m] = f32_to_bf16(hi);
+                    sm.tl[row][16 * j + m] = f32_to_bf16(lo);
+                }
+            }
+            __syncthreads();
+        }
+
+        // ---- state-dependent part (per wave, its value columns) --------------------
+        f32x4_t ks[P::NCT][P::NVT], qs[P::NCT][P::NVT];
+#pragma unroll
+        for (int ct = 0; ct < P::NCT; ++ct)
+#pragma unroll
+            for (int vt = 0; vt < P::NVT; ++vt) {
+                ks[ct][vt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+                qs[ct][vt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            }
+        float ones[4] = {1.f, 1.f, 1.f, 1.f};
+        // K S0^T (S0 hi + lo) and Q S0^T (S0 hi)
+#pragma unroll
+        for (int kk = 0; kk < D; kk += KD) {
+            FD bh[P::NVT], bl[P::NVT];
+#pragma unroll
+            for (int vt = 0; vt < P::NVT; ++vt)
+                acc_frag<KD>(st[kk / 16][vt], st[(kk / 16) + (KD == 32 ? 1 : 0)][vt], ones, ones, bh[vt], bl[vt]);
+#pragma unroll
+            for (int ct = 0; ct < P::NCT; ++ct) {
+                const FD ak = lds_frag_perm<KD>(&sm.k[16 * ct + m][0], kk, gq);
+                const FD aq = lds_frag_perm<KD>(&sm.q[16 * ct + m][0], kk, gq);
+#pragma unroll
+                for (int vt = 0; vt < P::NVT; ++vt) {
+                    ks[ct][vt] = mma(ak, bh[vt], ks[ct][vt]);
+                    ks[ct][vt] = mma(ak, bl[vt], ks[ct][vt]);
+                    qs[ct][vt] = mma(aq, bh[vt], qs[ct][vt]);
+                }
+            }
+        }
+        // W = V - diag(exp(gamma)) K S0^T   (in place of ks)
+        // O starts as diag(exp(gamma)) Q S0^T (in place of qs)
+        float egr[P::NCT][4];
+#pragma unroll
+        for (int ct = 0; ct < P::NCT; ++ct)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) egr[ct][i] = sm.eg[16 * ct + 4 * gq + i];
+#pragma unroll
+        for (int ct = 0; ct < P::NCT; ++ct)
+#pragma unroll
+            for (int vt = 0; vt < P::NVT; ++vt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float vv = bf16_to_f32(sm.v[16 * ct + 4 * gq + i][vcol0 + 16 * vt + m]);
+                    ks[ct][vt][i] = fmaf(-egr[ct][i], ks[ct][vt][i], vv);
+                    qs[ct][vt][i] *= egr[ct][i];
+                }
+        // U = T diag(beta) W   (three bf16 products: hi*hi + hi*lo + lo*hi)
+        f32x4_t uu[P::NCT][P::NVT];
+#pragma unroll
+        for (int ct = 0; ct < P::NCT; ++ct)
+#pragma unroll
+            for (int vt = 0; vt < P::NVT; ++vt) uu[ct][vt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kc = 0; kc < C; kc += KC) {
+            FC wh[P::NVT], wl[P::NVT];
+#pragma unroll
+            for (int vt = 0; vt < P::NVT; ++vt)
+                acc_frag<KC>(ks[kc / 16][vt], ks[(kc / 16) + (KC == 32 ? 1 : 0)][vt], ones, ones, wh[vt], wl[vt]);
+#pragma unroll
+            for (int ct = 0; ct < P::NCT; ++ct) {
+                if (kc > 16 * ct + 15) continue;  // block above the diagonal: zero
+                const FC ah = lds_frag_perm<KC>(&sm.th[16 * ct + m][0], kc, gq);
+                const FC al = lds_frag_perm<KC>(&sm.tl[16 * ct + m][0], kc, gq);
+#pragma unroll
+                for (int vt = 0; vt < P::NVT; ++vt) {
+                    uu[ct][vt] = mma(ah, wh[vt], uu[ct][vt]);
+                    uu[ct][vt] = mma(ah, wl[vt], uu[ct][vt]);
+                    uu[ct][vt] = mma(al, wh[vt], uu[ct][vt]);
+                }
+            }
+        }
+        // O += (M o Q K^T) U   (U hi); the state update operand diag(exp(gamma_last -
+        // gamma)) U is split into hi + lo.
+        float eglr[P::NCT][4];
+#pragma unroll
+        for (int ct = 0; ct < P::NCT; ++ct)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) eglr[ct][i] = sm.egl[16 * ct + 4 * gq + i];
+        const float eg_last = sm.eg[C - 1];
+        FC uth[C / KC][P::NVT], utl[C / KC][P::NVT];
+#pragma unroll
+        for (int kc = 0; kc < C; kc += KC) {
+            FC uh[P::NVT], ul[P::NVT];
+#pragma unroll
+            for (int vt = 0; vt < P::NVT; ++vt) {
+                const int c1 = (kc / 16) + (KC == 32 ? 1 : 0);
+                acc_frag<KC>(uu[kc / 16][vt], uu[c1][vt], ones, ones, uh[vt], ul[vt]);
+                acc_frag<KC>(uu[kc / 16][vt], uu[c1][vt], eglr[kc / 16], eglr[c1],
+                             uth[kc / KC][vt], utl[kc / KC][vt]);
+            }
+#pragma unroll
+            for (int ct = 0; ct < P::NCT; ++ct) {
+                if (kc > 16 * ct + 15) continue;
+                const FC ap = lds_frag_perm<KC>(&sm.pm[16 * ct + m][0], kc, gq);
+#pragma unroll
+                for (int vt = 0; vt < P::NVT; ++vt) qs[ct][vt] = mma(ap, uh[vt], qs[ct][vt]);
+            }
+        }
+        // S^T = exp(gamma_last) S^T + K^T (diag(exp(gamma_last - gamma)) U)   (hi + lo)
+#pragma unroll
+        for (int dt = 0; dt < P::NDT; ++dt) {
+#pragma unroll
+            for (int vt = 0; vt < P::NVT; ++vt) st[dt][vt] *= eg_last;
+#pragma unroll
+            for (int kc = 0; kc < C; kc += KC) {
+                const FC a = lds_frag_perm<KC>(&sm.kt[16 * dt + m][0], kc, gq);
+#pragma unroll
+                for (int vt = 0; vt < P::NVT; ++vt) {
+                    st[dt][vt] = mma(a, uth[kc / KC][vt], st[dt][vt]);
+                    st[dt][vt] = mma(a, utl[kc / KC][vt], st[dt][vt]);
+                }
+            }
+        }
+        // ---- outputs: stage in LDS, then coalesced 16-byte stores ------------------
+        // sm.u.o overlays the T scratch, which no wave reads after the last level
+        // barrier.  The barrier below also guarantees every wave has finished the
+        // state-dependent part before the next chunk is staged.
+#pragma unroll
+        for (int ct = 0; ct < P::NCT; ++ct)
+#pragma unroll
+            for (int vt = 0; vt < P::NVT; ++vt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    sm.u.o[16 * ct + 4 * gq + i][vcol0 + 16 * vt + m] = f32_to_bf16(scale * qs[ct][vt][i]);
+        __syncthreads();
+        for (int i = tid; i < L * (D / 8); i += P::NT) {
+            const int r = i / (D / 8), seg = i - r * (D / 8);
+            *reinterpret_cast<uint4*>(o + (size_t)(t0 + r) * v_stride + (size_t)h * D + seg * 8) =
+                *reinterpret_cast<const uint4*>(&sm.u.o[r][seg * 8]);
+        }
+        // No barrier: the next staging writes only q, k, v, graw and beta; sm.u is
+        // next written after the staging barrier.
+    }
+
+    // final state
+#pragma unroll
+    for (int dt = 0; dt < P::NDT; ++dt)
+#pragma unroll
+        for (int vt = 0; vt < P::NVT; ++vt) {
+            const float4 s4 = {st[dt][vt][0], st[dt][vt][1], st[dt][vt][2], st[dt][vt][3]};
+            *reinterpret_cast<float4*>(final_state + state_off + (size_t)(vcol0 + 16 * vt + m) * D +
+                                       16 * dt + 4 * gq) = s4;
+        }
+}
+
+size_t prefill_workspace_bytes(int N) {
+    return ((size_t)N * sizeof(int32_t) + 255) / 256 * 256;
+}
+
+template <int D, int C>
+static hipError_t launch_prefill_dc(const PrefillArgs& a, hipStream_t stream) {
+    int32_t* order = static_cast<int32_t*>(a.workspace);
+    hipLaunchKernelGGL(prefill_schedule_kernel, dim3(1), dim3(256), 0, stream, a.cu_seqlens, a.N, order);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((prefill_kernel<D, C>), dim3((unsigned)(a.N * a.H_v)), dim3(Cfg<D, C>::NT), 0,
+                       stream, (const uint16_t*)a.q, (const uint16_t*)a.k, (const uint16_t*)a.v, a.g,
+                       a.beta, a.cu_seqlens, (const int32_t*)order, a.initial_state, a.final_state,
+                       (uint16_t*)a.o, a.N, a.H_qk, a.H_v, a.scale);
+    return hipGetLastError();
+}
+
+hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {
+    if (a.D == 128) return launch_prefill_dc<128, 64>(a, stream);
+    return launch_prefill_dc<16, 16>(a, stream);
+}
+
+}  // namespace gdn

@@ -20,7 +20,9 @@ changing a bit.
 from __future__ import annotations
 
 import dataclasses
-from typing import Optional, Sequence
+import os
+from concurrent.futures import ThreadPoolExecutor
+from typing import Optional, Sequence, Tuple
 
 import numpy as np
 
@@ -29,6 +31,8 @@ __all__ = [
     "DecodeInputs",
     "PrefillInputs",
     "decode_inputs",
+    "decode_state",
+    "decode_step_inputs",
     "prefill_inputs",
     "varlen_lengths",
     "WORKLOADS",
@@ -46,14 +50,44 @@ def bf16_bits(x: np.ndarray) -> np.ndarray:
     return rounded.astype(np.uint16)
 
 
-def _rng(seed: int) -> np.random.Generator:
-    return np.random.Generator(np.random.Philox(seed))
+_BLOCK = 1 << 21  # elements per independently seeded block
 
 
-def _unit_rows(rng: np.random.Generator, shape) -> np.ndarray:
-    x = rng.standard_normal(shape, dtype=np.float32)
-    x /= np.linalg.norm(x, axis=-1, keepdims=True)
-    return x
+def _threads() -> int:
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+def _normal(entropy: Tuple[int, ...], shape, unit_last: bool = False, std: float = 1.0,
+            bf16: bool = False) -> np.ndarray:
+    """N(0, 1) draws of ``shape`` in fixed blocks of rows; block i is drawn from
+    PCG64(SeedSequence(entropy + (i,))), so the values do not depend on the
+    number of worker threads.  ``unit_last`` L2-normalises over the last axis;
+    ``std`` scales; ``bf16`` returns bf16 bit patterns (uint16)."""
+    shape = tuple(int(x) for x in shape)
+    n = int(np.prod(shape)) if shape else 1
+    row = shape[-1] if (unit_last and shape) else 1
+    block = max(row, (_BLOCK // row) * row)
+    out = np.empty(n, dtype=np.uint16 if bf16 else np.float32)
+    nblocks = (n + block - 1) // block
+
+    def work(i):
+        s, e = i * block, min(n, (i + 1) * block)
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(tuple(entropy) + (i,))))
+        x = rng.standard_normal(e - s, dtype=np.float32)
+        if unit_last:
+            x2 = x.reshape(-1, row)
+            x2 /= np.sqrt(np.einsum("ij,ij->i", x2, x2))[:, None]
+        if std != 1.0:
+            x *= np.float32(std)
+        out[s:e] = bf16_bits(x) if bf16 else x
+
+    if nblocks <= 1:
+        for i in range(nblocks):
+            work(i)
+    else:
+        with ThreadPoolExecutor(_threads()) as ex:
+            list(ex.map(work, range(nblocks)))
+    return out.reshape(shape)
 
 
 def _softplus(x: np.ndarray) -> np.ndarray:
@@ -62,6 +96,10 @@ def _softplus(x: np.ndarray) -> np.ndarray:
 
 def _sigmoid(x: np.ndarray) -> np.ndarray:
     return (1.0 / (1.0 + np.exp(-x))).astype(np.float32)
+
+
+# tensor tags mixed into the seeds
+_Q, _K, _V, _BETA, _G, _STATE, _LEN = 1, 2, 3, 4, 5, 6, 7
 
 
 @dataclasses.dataclass
@@ -107,25 +145,37 @@ class PrefillInputs:
 def decode_inputs(seed: int, B: int, H_qk: int, H_v: int, D: int,
                   state_std: float = 0.02, scale: float = 1.0,
                   qkv_dtype: str = "bf16") -> DecodeInputs:
-    """Draw one decode step.  ``qkv_dtype="f32"`` keeps q/k/v as fp32 (oracle-only use)."""
-    rng = _rng(seed)
-    q = _unit_rows(rng, (B, H_qk, D))
-    k = _unit_rows(rng, (B, H_qk, D))
-    v = rng.standard_normal((B, H_v, D), dtype=np.float32)
-    beta = _sigmoid(rng.standard_normal((B, H_v), dtype=np.float32))
-    g = -_softplus(rng.standard_normal((B, H_v), dtype=np.float32))
+    """Draw one decode step and its prior state.  ``qkv_dtype="f32"`` keeps
+    q/k/v as fp32 (oracle-only use)."""
+    step = decode_step_inputs(seed, 0, B, H_qk, H_v, D, qkv_dtype=qkv_dtype)
+    step.state = decode_state(seed, B, H_v, D, state_std)
+    step.scale = scale
+    return step
+
+
+def decode_state(seed: int, B: int, H_v: int, D: int, state_std: float = 0.02) -> np.ndarray:
+    """Prior decode state [B, H_v, D, D] fp32: std * N(0, 1), or zeros if std is 0."""
     if state_std == 0.0:
-        state = np.zeros((B, H_v, D, D), np.float32)
-    else:
-        state = (np.float32(state_std) * rng.standard_normal((B, H_v, D, D), dtype=np.float32))
-    if qkv_dtype == "bf16":
-        q, k, v = bf16_bits(q), bf16_bits(k), bf16_bits(v)
-    return DecodeInputs(q, k, v, g, beta, state, scale)
+        return np.zeros((B, H_v, D, D), np.float32)
+    return _normal((seed, _STATE), (B, H_v, D, D), std=state_std)
+
+
+def decode_step_inputs(seed: int, step: int, B: int, H_qk: int, H_v: int, D: int,
+                       qkv_dtype: str = "bf16") -> DecodeInputs:
+    """Fresh q, k, v, g, beta for decode step ``step`` (state left as None)."""
+    bf = qkv_dtype == "bf16"
+    q = _normal((seed, step, _Q), (B, H_qk, D), unit_last=True, bf16=bf)
+    k = _normal((seed, step, _K), (B, H_qk, D), unit_last=True, bf16=bf)
+    v = _normal((seed, step, _V), (B, H_v, D), bf16=bf)
+    beta = _sigmoid(_normal((seed, step, _BETA), (B, H_v)))
+    g = -_softplus(_normal((seed, step, _G), (B, H_v)))
+    return DecodeInputs(q, k, v, g, beta, None)
 
 
 def varlen_lengths(seed: int, N: int, lo: int, hi: int) -> np.ndarray:
     """N sequence lengths drawn uniformly from the integers in [lo, hi]."""
-    return _rng(seed + 7919).integers(lo, hi + 1, size=N).astype(np.int64)
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence((seed, _LEN))))
+    return rng.integers(lo, hi + 1, size=N).astype(np.int64)
 
 
 def prefill_inputs(seed: int, lengths: Sequence[int], H_qk: int, H_v: int, D: int,
@@ -138,17 +188,15 @@ def prefill_inputs(seed: int, lengths: Sequence[int], H_qk: int, H_v: int, D: in
     cu = np.zeros(N + 1, np.int64)
     np.cumsum(lengths, out=cu[1:])
     T = int(cu[-1])
-    rng = _rng(seed)
-    q = _unit_rows(rng, (T, H_qk, D))
-    k = _unit_rows(rng, (T, H_qk, D))
-    v = rng.standard_normal((T, H_v, D), dtype=np.float32)
-    beta = _sigmoid(rng.standard_normal((T, H_v), dtype=np.float32))
-    g = -_softplus(rng.standard_normal((T, H_v), dtype=np.float32))
+    bf = qkv_dtype == "bf16"
+    q = _normal((seed, _Q), (T, H_qk, D), unit_last=True, bf16=bf)
+    k = _normal((seed, _K), (T, H_qk, D), unit_last=True, bf16=bf)
+    v = _normal((seed, _V), (T, H_v, D), bf16=bf)
+    beta = _sigmoid(_normal((seed, _BETA), (T, H_v)))
+    g = -_softplus(_normal((seed, _G), (T, H_v)))
     init = None
     if state_std is not None:
-        init = (np.float32(state_std) * rng.standard_normal((N, H_v, D, D), dtype=np.float32))
-    if qkv_dtype == "bf16":
-        q, k, v = bf16_bits(q), bf16_bits(k), bf16_bits(v)
+        init = _normal((seed, _STATE), (N, H_v, D, D), std=state_std)
     return PrefillInputs(q, k, v, g, beta, cu.astype(np.int32), init, scale)
 
 

@@ -1,0 +1,137 @@
+"""The C ABI on a machine without a GPU: the library loads, exports every
+symbol include/gdn.h declares, and every argument check fails with its own
+status and message before any HIP call (so nothing is launched)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2607_17979_amd import gdn
+from paper_2607_17979_amd.build import LIB_PATH
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gdn.h")
+
+OK, EINVAL, EUNSUP, EALIGN, EWS, EHIP = 0, -1, -2, -3, -4, -5
+P = 0x10000  # a fake, 256-byte aligned "device" address: never dereferenced
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"GDN_API\s+[\w\s\*]+?\b(gdn_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return gdn.load_library()
+
+
+def test_header_declares_the_bound_symbols():
+    assert declared_symbols() == sorted(gdn.EXPORTED_SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_symbols():
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", LIB_PATH], capture_output=True, text=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if " T " in line}
+    gdn_exported = {s for s in exported if s.startswith("gdn_")}
+    assert gdn_exported == set(declared_symbols())
+
+
+def test_abi_version(lib):
+    assert lib.gdn_abi_version() == 100
+
+
+def decode(lib, q=P, k=P, v=P, g=P, beta=P, state=P, o=P, B=2, H_qk=1, H_v=2, Dk=128, Dv=128,
+           scale=1.0):
+    return lib.gdn_decode(q, k, v, g, beta, state, o, B, H_qk, H_v, Dk, Dv, scale, None)
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(B=-1), EINVAL, "B must be"),
+    (dict(H_qk=0), EINVAL, "head counts"),
+    (dict(H_qk=3, H_v=4), EINVAL, "multiple"),
+    (dict(Dk=64, Dv=64), EUNSUP, "head dim"),
+    (dict(Dk=128, Dv=16), EUNSUP, "must equal"),
+    (dict(q=None), EINVAL, "q is NULL"),
+    (dict(state=None), EINVAL, "state is NULL"),
+    (dict(o=P + 8), EALIGN, "o is not 16-byte"),
+    (dict(state=P + 4), EALIGN, "state is not 16-byte"),
+    (dict(g=P + 2), EALIGN, "g is not 4-byte"),
+])
+def test_decode_rejects(lib, kw, status, msg):
+    assert decode(lib, **kw) == status
+    assert msg in gdn.gdn_last_error()
+
+
+def test_decode_zero_batch_is_noop(lib):
+    assert decode(lib, q=None, k=None, v=None, g=None, beta=None, state=None, o=None, B=0) == OK
+    assert gdn.gdn_last_error() == ""
+
+
+def ws_size(lib, N=3, T=10, H_qk=1, H_v=2, D=128, chunk=64):
+    return lib.gdn_prefill_workspace_size(N, T, H_qk, H_v, D, D, chunk)
+
+
+def test_workspace_size(lib):
+    assert ws_size(lib) == 256
+    assert ws_size(lib, N=100) == 512
+    assert ws_size(lib, N=0) == 0
+    assert ws_size(lib, D=16, chunk=16) == 256
+    assert ws_size(lib, chunk=16) == 0
+    assert ws_size(lib, H_qk=3, H_v=4) == 0
+    assert ws_size(lib, N=-1) == 0
+
+
+def prefill(lib, q=P, k=P, v=P, g=P, beta=P, cu=P, init=None, fin=P, o=P, N=3, T=10, H_qk=1,
+            H_v=2, Dk=128, Dv=128, chunk=64, ws=P, ws_bytes=256):
+    return lib.gdn_prefill_varlen(q, k, v, g, beta, cu, init, fin, o, N, T, H_qk, H_v, Dk, Dv,
+                                  chunk, 1.0, ws, ws_bytes, None)
+
+
+STATE_BYTES = 3 * 2 * 128 * 128 * 4
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(N=-1), EINVAL, "must be >= 0"),
+    (dict(T=-5), EINVAL, "must be >= 0"),
+    (dict(H_qk=2, H_v=3), EINVAL, "multiple"),
+    (dict(Dk=32, Dv=32), EUNSUP, "head dim"),
+    (dict(chunk=32), EUNSUP, "chunk 32"),
+    (dict(Dk=16, Dv=16, chunk=64), EUNSUP, "chunk 64"),
+    (dict(cu=None), EINVAL, "cu_seqlens is NULL"),
+    (dict(cu=P + 2), EALIGN, "cu_seqlens"),
+    (dict(fin=None), EINVAL, "final_state is NULL"),
+    (dict(init=P + 4, fin=P + 0x100000), EALIGN, "initial_state"),
+    (dict(init=P, fin=P + 1024), EINVAL, "overlap"),
+    (dict(init=P + 2 * STATE_BYTES, fin=P + STATE_BYTES // 2 // 16 * 16 + 2 * STATE_BYTES), EINVAL, "overlap"),
+    (dict(q=None), EINVAL, "q is NULL"),
+    (dict(v=P + 8), EALIGN, "v is not"),
+    (dict(beta=None), EINVAL, "beta is NULL"),
+    (dict(ws=None), EWS, "workspace"),
+    (dict(ws_bytes=100), EWS, "256 bytes needed"),
+    (dict(ws=P + 16), EALIGN, "workspace"),
+])
+def test_prefill_rejects(lib, kw, status, msg):
+    assert prefill(lib, **kw) == status
+    assert msg in gdn.gdn_last_error()
+
+
+def test_prefill_zero_sequences_is_noop(lib):
+    assert prefill(lib, q=None, k=None, v=None, g=None, beta=None, cu=None, fin=None, o=None,
+                   N=0, T=0, ws=None, ws_bytes=0) == OK
+
+
+def test_error_message_is_per_call(lib):
+    assert decode(lib, B=-1) == EINVAL
+    assert gdn.gdn_last_error() != ""
+    assert decode(lib, q=None, k=None, v=None, g=None, beta=None, state=None, o=None, B=0) == OK
+    assert gdn.gdn_last_error() == ""
+
+
+def test_binding_raises_on_missing_library(tmp_path):
+    with pytest.raises(RuntimeError, match="missing"):
+        gdn.load_library(str(tmp_path / "nope.so"))

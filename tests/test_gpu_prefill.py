@@ -1,0 +1,188 @@
+"""gdn_prefill_varlen on the GPU (through the C ABI) against the fp64 oracle."""
+import numpy as np
+import pytest
+
+import oracle.gdn_ref as ref
+from gpu_helpers import (bf16_np, check_outputs, check_states, device, note, rel_frob_units, to_dev)
+from paper_2607_17979_amd import gdn
+from paper_2607_17979_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+def _prefill_gpu(inp, dev, scale=None, in_place=False, workspace=None):
+    import torch
+
+    N, T, H_qk, H_v, D = inp.shape
+    q, k, v = (to_dev(x, dev, bf16=True) for x in (inp.q, inp.k, inp.v))
+    g, b = to_dev(inp.g, dev), to_dev(inp.beta, dev)
+    cu = to_dev(inp.cu_seqlens, dev)
+    init = to_dev(inp.initial_state, dev)
+    if in_place:
+        assert init is not None
+        fin = init
+    else:
+        fin = torch.full((N, H_v, D, D), float("nan"), dtype=torch.float32, device=dev)
+    o = torch.full((T, H_v, D), float("nan"), dtype=torch.bfloat16, device=dev)
+    gdn.gdn_prefill_varlen(q, k, v, g, b, cu, init, fin, o,
+                           scale=inp.scale if scale is None else scale, workspace=workspace)
+    return o, fin
+
+
+def _full_oracle_check(inp, o, fin, what):
+    o_ref, s_ref = ref.prefill_varlen(inp.q, inp.k, inp.v, inp.g, inp.beta, inp.cu_seqlens,
+                                      inp.initial_state, scale=inp.scale)
+    check_outputs(bf16_np(o), o_ref, what)
+    check_states(fin.cpu().numpy(), s_ref, what)
+
+
+def test_prefill_tiny_chunk16():
+    """The tiny workload: one 64-token sequence, two heads, d = 16, chunk 16."""
+    dev = device()
+    w = wl.WORKLOADS["tiny"]
+    note("prefill tiny d=16 chunk=16")
+    inp = wl.prefill_inputs(w["seed"], [w["T"]], w["H_qk"], w["H_v"], w["D"])
+    o, fin = _prefill_gpu(inp, dev)
+    _full_oracle_check(inp, o, fin, "tiny")
+
+
+@pytest.mark.parametrize("D", [16, 128])
+@pytest.mark.parametrize("with_state", [False, True])
+@pytest.mark.parametrize("seed", [30, 31, 32])
+def test_prefill_ragged_small(D, with_state, seed):
+    """Ragged lengths around the chunk size (empty, 1, C-1, C, C+1, several
+    chunks) in one packed batch, GVA 2:1."""
+    dev = device()
+    C = 16 if D == 16 else 64
+    lengths = [0, 1, C - 1, C, C + 1, 2 * C + 2, 3 * C + 7]
+    note(f"prefill ragged D={D} state={with_state} seed={seed} lengths={lengths}")
+    inp = wl.prefill_inputs(seed, lengths, 2, 4, D, state_std=0.02 if with_state else None,
+                            scale=D ** -0.5)
+    o, fin = _prefill_gpu(inp, dev)
+    _full_oracle_check(inp, o, fin, f"ragged D={D}")
+
+
+def _sampled_check(inp, o, fin, units, what):
+    cu = inp.cu_seqlens
+    got = ref.prefill_units(inp.q, inp.k, inp.v, inp.g, inp.beta, cu, units, inp.initial_state,
+                            scale=inp.scale)
+    o_bits = bf16_np(o)
+    fin_np = fin.cpu().numpy()
+    worst_o, worst_s = 0.0, 0.0
+    for (n, h), (o_ref, s_ref) in got.items():
+        out = ref.to_f64(o_bits[cu[n]:cu[n + 1], h])
+        worst_o = max(worst_o, float(np.max(np.abs(out - o_ref))) if out.size else 0.0)
+        worst_s = max(worst_s, float(rel_frob_units(fin_np[n, h], s_ref)))
+    note(f"  {what}: {len(units)} units, outputs max-abs {worst_o:.3e}, "
+         f"states worst rel-Frobenius {worst_s:.3e}")
+    assert worst_o <= 2e-2
+    assert worst_s <= 1e-3
+
+
+@pytest.mark.parametrize("seed", [4, 14, 24])
+def test_prefill_varlen16_parity(seed):
+    """16 packed sequences, lengths uniform in [128, 2048], 32 value / 16 q/k
+    heads, d = 128, chunk 64, zero initial state.  The oracle follows every
+    head of four sequences and two heads of every other sequence."""
+    dev = device()
+    w = wl.WORKLOADS["prefill_varlen16"]
+    lengths = wl.varlen_lengths(seed, w["N"], w["len_lo"], w["len_hi"])
+    note(f"prefill varlen16 seed {seed} T={lengths.sum()}")
+    inp = wl.prefill_inputs(seed, lengths, w["H_qk"], w["H_v"], w["D"])
+    o, fin = _prefill_gpu(inp, dev)
+    units = [(n, h) for n in range(4) for h in range(w["H_v"])]
+    units += [(n, (7 * n + 3) % w["H_v"]) for n in range(4, w["N"])]
+    units += [(n, (11 * n + 20) % w["H_v"]) for n in range(4, w["N"])]
+    _sampled_check(inp, o, fin, units, "varlen16")
+
+
+def test_prefill_long_2x64k():
+    """Two 65,536-token sequences from a nonzero initial state; the oracle
+    follows two value heads (one q/k pair and one unpaired) per sequence over
+    all 65,536 tokens."""
+    dev = device()
+    w = wl.WORKLOADS["prefill_long2x64k"]
+    note("prefill long 2 x 65536")
+    inp = wl.prefill_inputs(w["seed"], [w["len"]] * w["N"], w["H_qk"], w["H_v"], w["D"],
+                            state_std=w["state_std"])
+    o, fin = _prefill_gpu(inp, dev)
+    units = [(0, 0), (0, 1), (1, 17), (1, 30)]
+    _sampled_check(inp, o, fin, units, "long 2x64k")
+
+
+def test_prefill_identity_gate_bitwise_and_zero_length():
+    """g = 0, beta = 0 leaves every state bit for bit; a zero-length sequence
+    returns its initial state bit for bit."""
+    dev = device()
+    inp = wl.prefill_inputs(40, [70, 0, 5], 2, 4, 128, state_std=0.3)
+    inp.g[:] = 0.0
+    inp.beta[:] = 0.0
+    o, fin = _prefill_gpu(inp, dev)
+    assert np.array_equal(fin.cpu().numpy(), inp.initial_state)
+    _full_oracle_check(inp, o, fin, "identity gate")
+
+
+def test_prefill_in_place_and_deterministic():
+    dev = device()
+    inp = wl.prefill_inputs(41, [200, 64, 1], 2, 4, 128, state_std=0.02)
+    o1, f1 = _prefill_gpu(inp, dev)
+    o2, f2 = _prefill_gpu(inp, dev, in_place=True)
+    import torch
+
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(f1, f2)
+    _full_oracle_check(inp, o1, f1, "in place")
+
+
+def test_prefill_gva_equals_repeated_heads_bitwise():
+    import torch
+
+    dev = device()
+    inp = wl.prefill_inputs(42, [150, 90], 2, 4, 128, state_std=0.02)
+    o1, f1 = _prefill_gpu(inp, dev)
+    rep = wl.PrefillInputs(np.repeat(inp.q, 2, axis=1), np.repeat(inp.k, 2, axis=1), inp.v, inp.g,
+                           inp.beta, inp.cu_seqlens, inp.initial_state, inp.scale)
+    o2, f2 = _prefill_gpu(rep, dev)
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(f1, f2)
+
+
+def test_prefill_schedule_is_longest_first():
+    """The workspace holds the sequence order, longest first, ties by index
+    (integer work: compared exactly)."""
+    import torch
+
+    dev = device()
+    lengths = [5, 130, 0, 130, 64, 1, 300, 5]
+    inp = wl.prefill_inputs(43, lengths, 1, 2, 128)
+    ws = torch.zeros(256, dtype=torch.uint8, device=dev)
+    _prefill_gpu(inp, dev, workspace=ws)
+    torch.cuda.synchronize()
+    order = ws.view(torch.int32)[:len(lengths)].cpu().numpy()
+    expect = sorted(range(len(lengths)), key=lambda i: (-lengths[i], i))
+    assert order.tolist() == expect
+
+
+def test_prefill_then_decode_continues_the_sequence():
+    """Prefill of the first 100 tokens, then 5 decode steps on its final state,
+    equals the oracle over all 105 tokens."""
+    import torch
+
+    dev = device()
+    full = wl.prefill_inputs(44, [105], 2, 4, 128, state_std=0.02)
+    head = wl.PrefillInputs(full.q[:100], full.k[:100], full.v[:100], full.g[:100],
+                            full.beta[:100], np.array([0, 100], np.int32), full.initial_state)
+    o_pre, fin = _prefill_gpu(head, dev)
+    outs = [bf16_np(o_pre)]
+    for t in range(100, 105):
+        q, k, v = (to_dev(x[t:t + 1], dev, bf16=True) for x in (full.q, full.k, full.v))
+        o = torch.empty(v.shape, dtype=torch.bfloat16, device=dev)
+        gdn.gdn_decode(q, k, v, to_dev(full.g[t:t + 1], dev), to_dev(full.beta[t:t + 1], dev), fin, o)
+        outs.append(bf16_np(o))
+    torch.cuda.synchronize()
+    o_ref, s_ref = ref.prefill_varlen(full.q, full.k, full.v, full.g, full.beta, full.cu_seqlens,
+                                      full.initial_state)
+    check_outputs(np.concatenate(outs), o_ref, "prefill+decode")
+    check_states(fin.cpu().numpy(), s_ref, "prefill+decode")
