@@ -91,48 +91,66 @@ __device__ __forceinline__ typename Frag<K>::type lds_frag_nat(const uint16_t* r
     }
 }
 
-__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
-    return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// Two fp32 -> packed bf16 pair (round to nearest even; one conversion instruction).
+__device__ __forceinline__ uint32_t cvt_pk(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
 }
 
-// Round x to bf16 hi and the residual x - hi to bf16 lo.
-__device__ __forceinline__ void split_bf16(float x, float& hi, float& lo) {
-    hi = bf16_to_f32(f32_to_bf16(x));
-    lo = x - hi;
+// hi = bf16(x), lo = bf16(x - hi) for a pair, each packed: x = hi + lo to ~2^-17.
+__device__ __forceinline__ void split_pair(float a, float b, uint32_t& hi, uint32_t& lo) {
+    hi = cvt_pk(a, b);
+    lo = cvt_pk(a - __uint_as_float(hi << 16), b - __uint_as_float(hi & 0xFFFF0000u));
 }
 
-// B operand from accumulator tiles t0 (contraction rows k0..k0+15) and t1
-// (rows k0+16..k0+31), hi part and lo residual, in the permuted order.
+// B operand (hi and lo parts) from accumulator tiles t0 (contraction rows
+// k0..k0+15) and t1 (rows k0+16..k0+31), in the permuted order.
 template <int K>
-__device__ __forceinline__ void acc_frag(const f32x4_t& t0, const f32x4_t& t1, float mul0[4],
-                                         float mul1[4], typename Frag<K>::type& hi,
-                                         typename Frag<K>::type& lo) {
-    float h[8], l[8];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) split_bf16(t0[i] * mul0[i], h[i], l[i]);
+__device__ __forceinline__ void acc_frag(const f32x4_t& t0, const f32x4_t& t1,
+                                         typename Frag<K>::type& hi, typename Frag<K>::type& lo) {
     if constexpr (K == 32) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) split_bf16(t1[i] * mul1[i], h[4 + i], l[4 + i]);
-        uint4 uh = {pack_bf16(h[0], h[1]), pack_bf16(h[2], h[3]), pack_bf16(h[4], h[5]),
-                    pack_bf16(h[6], h[7])};
-        uint4 ul = {pack_bf16(l[0], l[1]), pack_bf16(l[2], l[3]), pack_bf16(l[4], l[5]),
-                    pack_bf16(l[6], l[7])};
+        uint4 uh, ul;
+        split_pair(t0[0], t0[1], uh.x, ul.x);
+        split_pair(t0[2], t0[3], uh.y, ul.y);
+        split_pair(t1[0], t1[1], uh.z, ul.z);
+        split_pair(t1[2], t1[3], uh.w, ul.w);
         hi = __builtin_bit_cast(bf16x8_t, uh);
         lo = __builtin_bit_cast(bf16x8_t, ul);
     } else {
-        uint2 uh = {pack_bf16(h[0], h[1]), pack_bf16(h[2], h[3])};
-        uint2 ul = {pack_bf16(l[0], l[1]), pack_bf16(l[2], l[3])};
+        uint2 uh, ul;
+        split_pair(t0[0], t0[1], uh.x, ul.x);
+        split_pair(t0[2], t0[3], uh.y, ul.y);
         hi = __builtin_bit_cast(s16x4_t, uh);
         lo = __builtin_bit_cast(s16x4_t, ul);
     }
 }
 
+// B operand, hi part only.
+template <int K>
+__device__ __forceinline__ typename Frag<K>::type acc_frag_hi(const f32x4_t& t0, const f32x4_t& t1) {
+    if constexpr (K == 32) {
+        uint4 u = {cvt_pk(t0[0], t0[1]), cvt_pk(t0[2], t0[3]), cvt_pk(t1[0], t1[1]), cvt_pk(t1[2], t1[3])};
+        return __builtin_bit_cast(bf16x8_t, u);
+    } else {
+        uint2 u = {cvt_pk(t0[0], t0[1]), cvt_pk(t0[2], t0[3])};
+        return __builtin_bit_cast(s16x4_t, u);
+    }
+}
+
+// Round x to bf16 hi and the residual to lo (scalar form, for LDS stores).
+__device__ __forceinline__ void split_bf16(float x, uint16_t& hi, uint16_t& lo) {
+    hi = f32_to_bf16(x);
+    lo = f32_to_bf16(x - bf16_to_f32(hi));
+}
+
 // --- configuration -------------------------------------------------------------
 template <int D, int C>
 struct Cfg {
-    static constexpr int NW = (D == 128) ? 4 : 1;  // waves per workgroup
+    static constexpr int NW = (D == 128) ? 8 : 1;  // waves per workgroup (2 per SIMD for D = 128)
     static constexpr int NT = 64 * NW;             // threads
-    static constexpr int VW = D / NW;              // value columns per wave (32 or 16)
+    static constexpr int VW = D / NW;              // value columns per wave (16)
     static constexpr int NVT = VW / 16;            // 16-wide value tiles per wave
     static constexpr int NDT = D / 16;             // 16-row d tiles
     static constexpr int NCT = C / 16;             // 16-row chunk tiles
@@ -141,7 +159,10 @@ struct Cfg {
     static constexpr int PD = D + 8;               // LDS pitch (bf16) of [C][D] arrays
     static constexpr int PC = C + 8;               // LDS pitch (bf16) of [.][C] arrays
     static constexpr int PF = C + 4;               // LDS pitch (fp32) of [C][C] arrays
-    static_assert(NW == NCT, "one wave per diagonal 16x16 block of T");
+    static constexpr int SEGS = D / 8;             // 16-byte segments per q/k/v row
+    static constexpr int ITEMS = (C * SEGS + NT - 1) / NT;  // staged segments per thread
+    static_assert(NW >= NCT, "one wave per diagonal 16x16 block of T");
+    static_assert(NVT >= 1, "value tile of 16 columns");
 };
 
 template <int D, int C>
@@ -161,9 +182,9 @@ struct Smem {
         } f;
         uint16_t o[C][P::PD];   // output staging
     } u;
-    float gam[C];   // gamma (running sum of g)
-    float eg[C];    // exp(gamma)
-    float egl[C];   // exp(gamma_last - gamma)
+    alignas(16) float gam[C];   // gamma (running sum of g)
+    alignas(16) float eg[C];    // exp(gamma)
+    alignas(16) float egl[C];   // exp(gamma_last - gamma)
     float beta[C];
     float graw[C];
 };
@@ -258,32 +279,57 @@ __global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
     const size_t qk_stride = (size_t)H_qk * D;
     const size_t v_stride = (size_t)H_v * D;
 
+    // Chunk inputs are loaded into registers one chunk ahead (the loads of chunk
+    // c+1 are in flight while chunk c computes) and written to LDS at the top of
+    // the next iteration.  Rows past the sequence end are zero, with g = beta = 0.
+    uint4 pq[P::ITEMS], pk[P::ITEMS], pv[P::ITEMS];
+    float pg = 0.f, pb = 0.f;
+    auto load_chunk = [&](int cbeg) {
+        const int Lc = min(C, seq_len - cbeg);
+        const int tb = seq_beg + cbeg;
+#pragma unroll
+        for (int it = 0; it < P::ITEMS; ++it) {
+            const int i = tid + it * P::NT;
+            const int r = i / P::SEGS, seg = i - r * P::SEGS;
+            pq[it] = pk[it] = pv[it] = uint4{0, 0, 0, 0};
+            if (i < C * P::SEGS && r < Lc) {
+                const size_t tq = (size_t)(tb + r) * qk_stride + (size_t)hq * D + seg * 8;
+                pq[it] = *reinterpret_cast<const uint4*>(q + tq);
+                pk[it] = *reinterpret_cast<const uint4*>(k + tq);
+                pv[it] = *reinterpret_cast<const uint4*>(v + (size_t)(tb + r) * v_stride + (size_t)h * D + seg * 8);
+            }
+        }
+        if (tid < C) {
+            const bool in = tid < Lc;
+            pg = in ? g[(size_t)(tb + tid) * H_v + h] : 0.f;
+            pb = in ? beta[(size_t)(tb + tid) * H_v + h] : 0.f;
+        }
+    };
+    if (seq_len > 0) load_chunk(0);
+
     for (int c0 = 0; c0 < seq_len; c0 += C) {
         const int L = min(C, seq_len - c0);
         const int t0 = seq_beg + c0;
 
         // ---- stage the chunk ---------------------------------------------------
-        // (the previous iteration ended with a barrier; the output staging of the
-        // previous chunk lives in sm.u and is flushed below before sm.u is reused)
-        for (int i = tid; i < C * (D / 8); i += P::NT) {
-            const int r = i / (D / 8), seg = i - r * (D / 8);
-            uint4 qv = {0, 0, 0, 0}, kv = {0, 0, 0, 0}, vv = {0, 0, 0, 0};
-            if (r < L) {
-                const size_t tq = (size_t)(t0 + r) * qk_stride + (size_t)hq * D + seg * 8;
-                qv = *reinterpret_cast<const uint4*>(q + tq);
-                kv = *reinterpret_cast<const uint4*>(k + tq);
-                vv = *reinterpret_cast<const uint4*>(v + (size_t)(t0 + r) * v_stride + (size_t)h * D + seg * 8);
+        // No wave reads sm.q/k/v/graw/beta after the previous chunk's output
+        // barrier, so they can be overwritten here.
+#pragma unroll
+        for (int it = 0; it < P::ITEMS; ++it) {
+            const int i = tid + it * P::NT;
+            const int r = i / P::SEGS, seg = i - r * P::SEGS;
+            if (i < C * P::SEGS) {
+                *reinterpret_cast<uint4*>(&sm.q[r][seg * 8]) = pq[it];
+                *reinterpret_cast<uint4*>(&sm.k[r][seg * 8]) = pk[it];
+                *reinterpret_cast<uint4*>(&sm.v[r][seg * 8]) = pv[it];
             }
-            *reinterpret_cast<uint4*>(&sm.q[r][seg * 8]) = qv;
-            *reinterpret_cast<uint4*>(&sm.k[r][seg * 8]) = kv;
-            *reinterpret_cast<uint4*>(&sm.v[r][seg * 8]) = vv;
         }
-        for (int i = tid; i < C; i += P::NT) {
-            const bool in = i < L;
-            sm.graw[i] = in ? g[(size_t)(t0 + i) * H_v + h] : 0.f;
-            sm.beta[i] = in ? beta[(size_t)(t0 + i) * H_v + h] : 0.f;
+        if (tid < C) {
+            sm.graw[tid] = pg;
+            sm.beta[tid] = pb;
         }
         __syncthreads();
+        if (c0 + C < seq_len) load_chunk(c0 + C);
 
         // ---- gate prefix, K^T, raw score tiles -----------------------------------
         if (wave == 0) {
@@ -365,7 +411,7 @@ __global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
         // ---- T = (I + A)^-1 -------------------------------------------------------
         // diagonal blocks by forward substitution: wave w, lane j < 16 -> column j
         // of block w.
-        {
+        if (wave < P::NCT) {
             const int b = wave;
             float x[16];
 #pragma unroll
@@ -380,10 +426,7 @@ __global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     sm.u.f.t[16 * b + r][16 * b + m] = x[r];
-                    float hi, lo;
-                    split_bf16(x[r] * bcol, hi, lo);
-                    sm.th[16 * b + r][16 * b + m] = f32_to_bf16(hi);
-                    sm.tl[16 * b + r][16 * b + m] = f32_to_bf16(lo);
+                    split_bf16(x[r] * bcol, sm.th[16 * b + r][16 * b + m], sm.tl[16 * b + r][16 * b + m]);
                 }
             }
         }
@@ -393,7 +436,7 @@ __global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
         for (int lev = 1; lev < P::NCT; ++lev) {
             const int j = wave;
             const int b = j + lev;
-            if (b < P::NCT) {
+            if (b < P::NCT) {  // waves j < NCT - lev; the others only meet the barrier
                 f32x4_t y = {0.f, 0.f, 0.f, 0.f};
                 for (int kb = j; kb < b; ++kb) {
 #pragma unroll
@@ -412,10 +455,7 @@ __global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
                 for (int i = 0; i < 4; ++i) {
                     const int row = 16 * b + 4 * gq + i;
                     sm.u.f.t[row][16 * j + m] = z[i];
-                    float hi, lo;
-                    split_bf16(z[i] * bcol, hi, lo);
-                    sm.th[row][16 * j + m] = f32_to_bf16(hi);
-                    sm.tl[row][16 * j + m] = f32_to_bf16(lo);
+                    split_bf16(z[i] * bcol, sm.th[row][16 * j + m], sm.tl[row][16 * j + m]);
                 }
             }
             __syncthreads();
@@ -430,14 +470,13 @@ __global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
                 ks[ct][vt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
                 qs[ct][vt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
             }
-        float ones[4] = {1.f, 1.f, 1.f, 1.f};
         // K S0^T (S0 hi + lo) and Q S0^T (S0 hi)
 #pragma unroll
         for (int kk = 0; kk < D; kk += KD) {
             FD bh[P::NVT], bl[P::NVT];
 #pragma unroll
             for (int vt = 0; vt < P::NVT; ++vt)
-                acc_frag<KD>(st[kk / 16][vt], st[(kk / 16) + (KD == 32 ? 1 : 0)][vt], ones, ones, bh[vt], bl[vt]);
+                acc_frag<KD>(st[kk / 16][vt], st[(kk / 16) + (KD == 32 ? 1 : 0)][vt], bh[vt], bl[vt]);
 #pragma unroll
             for (int ct = 0; ct < P::NCT; ++ct) {
                 const FD ak = lds_frag_perm<KD>(&sm.k[16 * ct + m][0], kk, gq);
@@ -452,11 +491,9 @@ __global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
         }
         // W = V - diag(exp(gamma)) K S0^T   (in place of ks)
         // O starts as diag(exp(gamma)) Q S0^T (in place of qs)
-        float egr[P::NCT][4];
+        f32x4_t egr[P::NCT];
 #pragma unroll
-        for (int ct = 0; ct < P::NCT; ++ct)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) egr[ct][i] = sm.eg[16 * ct + 4 * gq + i];
+        for (int ct = 0; ct < P::NCT; ++ct) egr[ct] = *reinterpret_cast<const f32x4_t*>(&sm.eg[16 * ct + 4 * gq]);
 #pragma unroll
         for (int ct = 0; ct < P::NCT; ++ct)
 #pragma unroll
@@ -478,7 +515,7 @@ __global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
             FC wh[P::NVT], wl[P::NVT];
 #pragma unroll
             for (int vt = 0; vt < P::NVT; ++vt)
-                acc_frag<KC>(ks[kc / 16][vt], ks[(kc / 16) + (KC == 32 ? 1 : 0)][vt], ones, ones, wh[vt], wl[vt]);
+                acc_frag<KC>(ks[kc / 16][vt], ks[(kc / 16) + (KC == 32 ? 1 : 0)][vt], wh[vt], wl[vt]);
 #pragma unroll
             for (int ct = 0; ct < P::NCT; ++ct) {
                 if (kc > 16 * ct + 15) continue;  // block above the diagonal: zero
@@ -494,22 +531,21 @@ __global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
         }
         // O += (M o Q K^T) U   (U hi); the state update operand diag(exp(gamma_last -
         // gamma)) U is split into hi + lo.
-        float eglr[P::NCT][4];
+        f32x4_t eglv[P::NCT];
 #pragma unroll
         for (int ct = 0; ct < P::NCT; ++ct)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) eglr[ct][i] = sm.egl[16 * ct + 4 * gq + i];
+            eglv[ct] = *reinterpret_cast<const f32x4_t*>(&sm.egl[16 * ct + 4 * gq]);
         const float eg_last = sm.eg[C - 1];
         FC uth[C / KC][P::NVT], utl[C / KC][P::NVT];
 #pragma unroll
         for (int kc = 0; kc < C; kc += KC) {
-            FC uh[P::NVT], ul[P::NVT];
+            const int c1 = (kc / 16) + (KC == 32 ? 1 : 0);
+            FC uh[P::NVT];
 #pragma unroll
             for (int vt = 0; vt < P::NVT; ++vt) {
-                const int c1 = (kc / 16) + (KC == 32 ? 1 : 0);
-                acc_frag<KC>(uu[kc / 16][vt], uu[c1][vt], ones, ones, uh[vt], ul[vt]);
-                acc_frag<KC>(uu[kc / 16][vt], uu[c1][vt], eglr[kc / 16], eglr[c1],
-                             uth[kc / KC][vt], utl[kc / KC][vt]);
+                uh[vt] = acc_frag_hi<KC>(uu[kc / 16][vt], uu[c1][vt]);
+                acc_frag<KC>(uu[kc / 16][vt] * eglv[kc / 16], uu[c1][vt] * eglv[c1], uth[kc / KC][vt],
+                             utl[kc / KC][vt]);
             }
 #pragma unroll
             for (int ct = 0; ct < P::NCT; ++ct) {
