@@ -5,12 +5,12 @@
 One step of the default workload is one pass of the whole hot path over one
 batch of synthetic input:
   * gdn_decode on a batch of 64 sequences (32 value heads sharing 16 q/k heads,
-    d = 128, fp32 states [64, 32, 128, 128] updated in place), and
+    d = 128, fp32 states [64, 32, 128, 128] updated in place), launched once
+    for each of four independent state buffers (the decode states of four
+    layers, 4 x 128 MiB, more than the 256 MB last-level cache holds), and
   * gdn_prefill_varlen on 16 packed sequences with lengths uniform in
     [128, 2048] (same heads, chunk 64, zero initial states).
-Inputs are resident in HBM before timing starts.  Decode cycles through four
-independent state buffers (4 x 128 MiB) so that successive steps cannot be
-served from the 256 MB last-level cache.
+Inputs are resident in HBM before timing starts.
 
 The JSON line's ``value`` is the decode kernel's achieved HBM bandwidth
 (algorithmic bytes / kernel time, HIP events on the launch stream); the
@@ -59,6 +59,23 @@ def prefill_bytes(T, N, H_qk, H_v, D, init_state):
 
 # --- helpers ---------------------------------------------------------------------
 
+def measured_traffic(kernel: str):
+    """HBM bytes per launch of ``kernel`` from profiles/hbm_traffic.txt (FETCH_SIZE +
+    WRITE_SIZE from rocprofv3, scaled by a plain-copy calibration), or None when
+    the kernel's source has changed since those counters were taken."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.txt")
+    try:
+        rec = json.load(open(path))[kernel]
+        src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+    except (OSError, KeyError, ValueError):
+        return None
+    if hashlib.sha256(src).hexdigest()[:16] != rec.get("source_sha256_16"):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
 def _dev_inputs_decode(d, dev):
     from paper_2607_17979_amd.workloads import to_torch
 
@@ -75,7 +92,12 @@ def _dev_inputs_prefill(p, dev):
 
 
 class Decode:
-    def __init__(self, dev, B, H_qk, H_v, D, seed, nbuf):
+    """``per_step`` decode launches per call, each on the next of ``nbuf`` state
+    buffers (independent layers of a model), so successive launches cannot be
+    served from the last-level cache and the event pair around the call
+    amortises its own overhead."""
+
+    def __init__(self, dev, B, H_qk, H_v, D, seed, nbuf, per_step=1):
         import torch
         from paper_2607_17979_amd import workloads as wl
 
@@ -85,15 +107,17 @@ class Decode:
         self.states = [wl.to_torch(self.host.state, dev) for _ in range(nbuf)]
         self.o = torch.empty((B, H_v, D), dtype=torch.bfloat16, device=dev)
         self.i = 0
+        self.per_step = per_step
         self.bytes = decode_bytes(B, H_qk, H_v, D)
 
     def __call__(self):
         from paper_2607_17979_amd import gdn
 
         x = self.x
-        gdn.gdn_decode(x["q"], x["k"], x["v"], x["g"], x["beta"], self.states[self.i % len(self.states)],
-                       self.o)
-        self.i += 1
+        for _ in range(self.per_step):
+            gdn.gdn_decode(x["q"], x["k"], x["v"], x["g"], x["beta"],
+                           self.states[self.i % len(self.states)], self.o)
+            self.i += 1
 
 
 class Prefill:
@@ -195,7 +219,7 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="decode_b64+prefill_varlen16",
                     choices=["decode_b64+prefill_varlen16", "decode_b64", "decode_sweep",
-                             "prefill_varlen16", "prefill_long2x64k"])
+                             "prefill_varlen16", "prefill_long2x64k", "copy_calibration"])
     ap.add_argument("--batch", type=int, default=None, help="decode_sweep: one batch size only")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args(argv)
@@ -219,19 +243,24 @@ def main(argv=None):
     out = dict(metric=METRIC, n_gpus=1, steps=args.steps, warmup=args.warmup,
                higher_is_better=True, scaling="weak", vs_baseline=None, data="synthetic")
     print(f"# bench {args.workload}: setting up inputs", file=sys.stderr, flush=True)
+    if args.workload == "copy_calibration":
+        # A plain device-to-device copy of a known size: the reference for scaling
+        # the FETCH_SIZE / WRITE_SIZE counters into HBM bytes.
+        nbytes = 1 << 30
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        ms_step, per = _time_parts([lambda: dst.copy_(src)], args.steps, args.warmup)
+        gbs = 2 * nbytes / (per[0] * 1e-3) / 1e9
+        out.update(value=gbs, unit="GB/s", ms_per_step=ms_step, dtype="f32",
+                   config=dict(workload="copy_calibration", bytes_read=nbytes, bytes_written=nbytes))
+        print(json.dumps(out), flush=True)
+        return 0
 
-    if args.workload in ("decode_b64+prefill_varlen16", "decode_b64", "decode_sweep"):
-        if args.workload == "decode_sweep":
-            w = W["decode_sweep"]
-            batches = [args.batch] if args.batch else list(w["batches"])
-        else:
-            w = W["decode_b64"]
-            batches = [w["B"]]
     parts, names = [], []
     dec = pre = None
     if args.workload in ("decode_b64+prefill_varlen16", "decode_b64"):
         w = W["decode_b64"]
-        dec = Decode(dev, w["B"], w["H_qk"], w["H_v"], w["D"], w["seed"], nbuf=4)
+        dec = Decode(dev, w["B"], w["H_qk"], w["H_v"], w["D"], w["seed"], nbuf=4, per_step=4)
         parts.append(dec)
         names.append("decode")
     if args.workload in ("decode_b64+prefill_varlen16", "prefill_varlen16"):
@@ -249,6 +278,7 @@ def main(argv=None):
 
     if args.workload == "decode_sweep":
         w = W["decode_sweep"]
+        batches = [args.batch] if args.batch else list(w["batches"])
         lines = []
         for B in batches:
             nbuf = max(1, min(4, (512 << 20) // (B * w["H_v"] * w["D"] * w["D"] * 4)))
@@ -275,13 +305,15 @@ def main(argv=None):
     out["ms_per_step"] = ms_step
     cfg = {}
     if dec is not None:
+        times["decode"] /= dec.per_step  # per launch
         gbs = dec.bytes / (times["decode"] * 1e-3) / 1e9
         out.update(value=gbs, unit="GB/s", dtype="f32")
         out["roofline"] = dict(bound="hbm", achieved=gbs, peak=HBM_PEAK_GBS, unit="GB/s",
-                               frac=gbs / HBM_PEAK_GBS, traffic=None,
-                               kernel="gdn::decode_kernel<128,4>",
+                               frac=gbs / HBM_PEAK_GBS, traffic=measured_traffic("decode_kernel"),
+                               kernel="gdn::decode_kernel<128,1>",
                                bytes_per_launch=dec.bytes, us_per_launch=times["decode"] * 1e3)
-        cfg["decode"] = dict(B=dec.B, H_qk=dec.H_qk, H_v=dec.H_v, d=dec.D, state_buffers=len(dec.states))
+        cfg["decode"] = dict(B=dec.B, H_qk=dec.H_qk, H_v=dec.H_v, d=dec.D, state_buffers=len(dec.states),
+                             launches_per_step=dec.per_step)
     if pre is not None:
         t = times["prefill"] * 1e-3
         tflops = pre.flops / t / 1e12
@@ -289,7 +321,8 @@ def main(argv=None):
                     algorithmic_tflops=tflops, mfma_util=tflops / BF16_PEAK_TFLOPS,
                     hbm_GBs=pre.bytes / t / 1e9,
                     roofline=dict(bound="mfma", achieved=tflops, peak=BF16_PEAK_TFLOPS,
-                                  unit="TFLOP/s", frac=tflops / BF16_PEAK_TFLOPS, traffic=None,
+                                  unit="TFLOP/s", frac=tflops / BF16_PEAK_TFLOPS,
+                                  traffic=measured_traffic("prefill_kernel"),
                                   kernel="gdn::prefill_kernel<128,64> (+ schedule kernel)",
                                   flops_per_launch=pre.flops))
         out["prefill"] = pobj

@@ -18,8 +18,9 @@
 // j * LPR + c (c = lane % LPR).  For D = 128 a group of 8 lanes covers one
 // 512-byte row with four fully used 128-byte segments, 8 rows per wave
 // instruction, RS row sets per wave.  A workgroup of W waves covers
-// W * RS * (64 / LPR) consecutive rows of one head; the host picks RS and W so
-// that small batches still launch enough workgroups to fill the chip.
+// W * RS * (64 / LPR) consecutive rows of one head; the host picks W so that
+// small batches still launch enough workgroups to fill the chip.  State loads
+// and stores are non-temporal: every state is touched once per step.
 #include "gdn_device.h"
 #include "gdn_launch.h"
 
@@ -75,13 +76,14 @@ __global__ __launch_bounds__(256) void decode_kernel(
     uint16_t* op = o + (size_t)head * D;
 
     // Issue every state load of this lane before any arithmetic.
-    float4 s[RS][J];
+    f32x4_t s[RS][J];
 #pragma unroll
     for (int r = 0; r < RS; ++r) {
         const int row = row0 + r * RPI + sub;
 #pragma unroll
         for (int j = 0; j < J; ++j)
-            s[r][j] = *reinterpret_cast<const float4*>(sp + (size_t)row * D + (j * LPR + c) * 4);
+            s[r][j] = __builtin_nontemporal_load(
+                reinterpret_cast<const f32x4_t*>(sp + (size_t)row * D + (j * LPR + c) * 4));
     }
     float vi[RS];
 #pragma unroll
@@ -92,61 +94,45 @@ __global__ __launch_bounds__(256) void decode_kernel(
         const int row = row0 + r * RPI + sub;
         float kv = 0.f, sq = 0.f;
 #pragma unroll
-        for (int j = 0; j < J; ++j) {
-            kv = fmaf(s[r][j].x, kf[j][0], kv); sq = fmaf(s[r][j].x, qf[j][0], sq);
-            kv = fmaf(s[r][j].y, kf[j][1], kv); sq = fmaf(s[r][j].y, qf[j][1], sq);
-            kv = fmaf(s[r][j].z, kf[j][2], kv); sq = fmaf(s[r][j].z, qf[j][2], sq);
-            kv = fmaf(s[r][j].w, kf[j][3], kv); sq = fmaf(s[r][j].w, qf[j][3], sq);
-        }
+        for (int j = 0; j < J; ++j)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                kv = fmaf(s[r][j][e], kf[j][e], kv);
+                sq = fmaf(s[r][j][e], qf[j][e], sq);
+            }
         kv = group_sum<LPR>(kv);
         sq = group_sum<LPR>(sq);
         const float u = bt * (vi[r] - alpha * kv);
 #pragma unroll
         for (int j = 0; j < J; ++j) {
-            float4 n;
-            n.x = fmaf(alpha, s[r][j].x, u * kf[j][0]);
-            n.y = fmaf(alpha, s[r][j].y, u * kf[j][1]);
-            n.z = fmaf(alpha, s[r][j].z, u * kf[j][2]);
-            n.w = fmaf(alpha, s[r][j].w, u * kf[j][3]);
-            *reinterpret_cast<float4*>(sp + (size_t)row * D + (j * LPR + c) * 4) = n;
+            f32x4_t nv;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) nv[e] = fmaf(alpha, s[r][j][e], u * kf[j][e]);
+            __builtin_nontemporal_store(nv, reinterpret_cast<f32x4_t*>(sp + (size_t)row * D + (j * LPR + c) * 4));
         }
         if (c == 0) op[row] = f32_to_bf16(scale * fmaf(alpha, sq, u * kq));
     }
 }
 
-// Rows per workgroup = nwave * RS * (64 / LPR).  Big batches: a whole head per
-// 4-wave workgroup.  Small batches: split each head over several workgroups so
-// at least ~512 are in flight.
+// Rows per workgroup = nwave * RS * (64 / LPR).  With D = 128 a workgroup of
+// four waves covers 32 rows (16 KiB of state): of the tile shapes measured for
+// in-place streaming with non-temporal loads and stores (8 to 64 KiB per
+// workgroup), this one ran fastest.  Below 128 heads each workgroup is a single
+// wave (8 rows) so that at least ~500 workgroups are in flight.
 template <int D>
 static hipError_t launch_decode_d(const DecodeArgs& a, hipStream_t stream) {
     constexpr int F4_ROW = D / 4;
     constexpr int LPR = F4_ROW < 8 ? F4_ROW : 8;
     constexpr int RPI = 64 / LPR;
     const long heads = (long)a.B * a.H_v;
-    int rs, nwave;
-    if (D == 16) {
-        rs = 1; nwave = 1;                 // 16 rows: one wave per head
-    } else if (heads >= 512) {
-        rs = 4; nwave = 4;                 // 128 rows per workgroup
-    } else if (heads >= 128) {
-        rs = 4; nwave = 1;                 // 32 rows per workgroup
-    } else {
-        rs = 1; nwave = 1;                 // 8 rows per workgroup
-    }
-    const int rows_per_block = nwave * rs * RPI;
+    const int nwave = (D == 128 && heads >= 128) ? 4 : 1;
+    const int rows_per_block = nwave * RPI;
     const int blocks_per_head = D / rows_per_block;
     const dim3 grid((unsigned)(heads * blocks_per_head));
     const dim3 block(64 * nwave);
-#define GDN_DECODE_LAUNCH(RSV)                                                               \
-    hipLaunchKernelGGL((decode_kernel<D, RSV>), grid, block, 0, stream,                       \
-                       (const uint16_t*)a.q, (const uint16_t*)a.k, (const uint16_t*)a.v, a.g, \
-                       a.beta, a.state, (uint16_t*)a.o, a.H_qk, a.H_v, blocks_per_head, a.scale)
-    if (rs == 4) {
-        if constexpr (D / RPI >= 4) GDN_DECODE_LAUNCH(4);
-    } else {
-        GDN_DECODE_LAUNCH(1);
-    }
-#undef GDN_DECODE_LAUNCH
+    hipLaunchKernelGGL((decode_kernel<D, 1>), grid, block, 0, stream, (const uint16_t*)a.q,
+                       (const uint16_t*)a.k, (const uint16_t*)a.v, a.g, a.beta, a.state,
+                       (uint16_t*)a.o, a.H_qk, a.H_v, blocks_per_head, a.scale);
     return hipGetLastError();
 }
 
