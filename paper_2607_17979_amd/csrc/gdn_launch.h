@@ -37,6 +37,9 @@ struct PrefillArgs {
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
 hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream);
+// d = 128, chunk 64: the pipelined kernel (gdn_prefill_pipe.hip); `order` is the
+// longest-first schedule already written to the workspace.
+hipError_t launch_prefill_pipe(const PrefillArgs& a, const int32_t* order, hipStream_t stream);
 
 // Workspace layout of the prefill: int32 order[N] (sequence indices sorted by
 // length, longest first, ties by index), rounded up to 256 bytes.
