@@ -30,6 +30,7 @@ def compile_flags():
         "-fvisibility=hidden",
         "-Wall",
         "-Wno-unused-function",
+        "-Wshadow",
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
         "-I", os.path.join(ROOT, "include"),
     ]

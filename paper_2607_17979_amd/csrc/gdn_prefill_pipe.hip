@@ -11,13 +11,14 @@
 //   * 4 state waves: wave w owns value columns [32 w, 32 w + 32) of S^T in
 //     fp32 MFMA accumulators and, in iteration c, runs the state-dependent
 //     part of chunk c;
-//   * 4 producer waves: in iteration c they build K^T of chunk c (which the
-//     state waves need last) and then prepare every state-independent input of
-//     chunk c + 1, loading chunk c + 2 into registers meanwhile.
+//   * 4 producer waves: in iteration c they prepare every state-independent
+//     input of chunk c + 1, loading chunk c + 2 into registers meanwhile.
 //
 // One workgroup barrier ends each iteration.  Inside an iteration the roles
-// meet only through LDS counters: producers count "K^T of chunk c written",
-// state waves count "done reading Q of chunk c" and "done reading V of chunk c"
+// meet only through LDS counters: state waves count "K^T of chunk c written"
+// (each builds a part at the start of the iteration; all parts are needed by
+// the state update at its end), "done reading Q of chunk c" and "done reading
+// V of chunk c"
 // (Q and V have a single LDS buffer), and producers synchronise among
 // themselves with a counter barrier.  Buffers written by producers for chunk
 // c + 1 while state waves read chunk c (K, T diag(beta) hi/lo, the masked
@@ -37,16 +38,15 @@ constexpr int NDT = D / 16, NCT = C / 16;
 constexpr int PD = D + 8;             // LDS pitch (bf16) of [C][D] and [D][C] arrays
 constexpr int PC = C + 8;
 constexpr int BP = 24;                // pitch (bf16) of a stored 16 x 16 block
-constexpr int FP = 17;                // pitch (fp32) of a stored 16 x 16 block
+constexpr int FB = 20;                // row pitch (fp32) of a stored 16 x 16 block (16-byte rows)
+constexpr int FS = 16 * FB + 8;       // block stride (fp32): successive blocks start 8 banks apart
 constexpr int NBLK = NCT * (NCT + 1) / 2;   // lower-triangular 16 x 16 blocks (10)
 constexpr int SEGS = D / 8;                 // 16-byte segments per q/k/v row
 constexpr int PITEMS = C * SEGS / (64 * NP);  // staged segments per producer thread
 constexpr int kSpinLimit = 1 << 20;
 
 __device__ __forceinline__ constexpr int bidx(int i, int j) { return i * (i + 1) / 2 + j; }
-// Private slot of diagonal block b (b >= w) for producer wave w < 3: wave 0 uses
-// slots 0-3, wave 1 slots 4-6, wave 2 slots 7-8.
-__device__ __forceinline__ constexpr int dslot(int w, int b) { return 4 * w - w * (w - 1) / 2 + (b - w); }
+
 
 struct Smem {
     uint16_t kb[2][C][PD];            // K rows, by chunk parity
@@ -57,16 +57,35 @@ struct Smem {
     uint16_t tl[2][NBLK][16][BP];     // T diag(beta), bf16 lo
     uint16_t pm[2][NBLK][16][BP];     // (M o Q K^T), bf16
     uint16_t zero[16][BP];            // stands in for blocks above the diagonal
-    float a[NBLK][16][FP];            // A (strictly lower), producers only
-    float t[NBLK][16][FP];            // diagonal blocks of T, private slots per producer wave
-    float gam[NP][C];                 // per producer wave: gate prefix of its chunk
-    float bet[NP][C];                 // per producer wave: beta of its chunk
+    float at[NBLK][FS];               // A^T by lower blocks: at[blk][c * FB + r] = A[r][c] (producers)
+    float dtr[NCT][FS];               // D_b^T of the diagonal blocks of T (producers)
+    alignas(16) float gam[NP][C];     // per producer wave: gate prefix of its chunk
+    alignas(16) float bet[NP][C];     // per producer wave: beta of its chunk
     alignas(16) float eg[2][C];       // exp(gamma), by chunk parity
     alignas(16) float egl[2][C];      // exp(gamma_last - gamma), by chunk parity
-    unsigned cnt[4];                  // producer barrier, K^T ready, Q free, V free
+    unsigned cnt[4];                  // producer barrier, K^T written, Q free, V free
 };
 
 enum { CNT_PBAR = 0, CNT_KT = 1, CNT_QFREE = 2, CNT_VFREE = 3 };
+
+// Inclusive prefix sum over the 64 lanes of a wave (DPP row shifts, then row
+// broadcasts across the four rows of 16 lanes).
+template <int CTRL, int ROWMASK, bool BOUND>
+__device__ __forceinline__ float dpp_src(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, ROWMASK, 0xF, BOUND));
+}
+__device__ __forceinline__ float wave_prefix_sum(float x) {
+    x += dpp_src<0x111, 0xF, true>(x);  // row_shr:1
+    x += dpp_src<0x112, 0xF, true>(x);  // row_shr:2
+    x += dpp_src<0x114, 0xF, true>(x);  // row_shr:4
+    x += dpp_src<0x118, 0xF, true>(x);  // row_shr:8
+    x += dpp_src<0x142, 0xA, false>(x); // row_bcast:15 into rows 1 and 3
+    x += dpp_src<0x143, 0xC, false>(x); // row_bcast:31 into rows 2 and 3
+    return x;
+}
+
+// Row / column block of the lower-triangular block with linear index tri.
+__device__ __forceinline__ int tri_row(int tri) { return tri >= 6 ? 3 : tri >= 3 ? 2 : tri >= 1 ? 1 : 0; }
 
 // Count this wave (lane 0) into *ctr.  The compiler fence keeps the wave's
 // earlier LDS accesses before the increment; the LDS executes them in order.
@@ -97,6 +116,89 @@ __device__ __forceinline__ bf16x8_t blk_frag(const uint16_t (*blocks)[16][BP], c
     const uint2 hi = *reinterpret_cast<const uint2*>(p1);
     uint4 u = {lo.x, lo.y, hi.x, hi.y};
     return __builtin_bit_cast(bf16x8_t, u);
+}
+
+// Block column J of T below the diagonal (producer wave J):
+//     T_bJ = -D_b sum_{kb=J}^{b-1} A_{b,kb} T_{kb,J},   T_JJ = D_J,
+// each result kept in its accumulator, which as a B operand supplies
+// contraction row 4 g + s at step s.  All LDS operands are loaded first; the
+// results go out as T diag(beta) hi / lo.
+// 16 x 16 x 16 product of fp32 operands on bf16 MFMA with each operand split
+// into hi + lo (hi*hi + hi*lo + lo*hi; relative error ~2^-16).  a[j] is the A
+// operand (row m, contraction 4 g + j), b[j] the B operand (contraction 4 g + j,
+// column m); an accumulator holding X is the B operand of X and, read as
+// a[j], the A operand of X^T.
+__device__ __forceinline__ f32x4_t prod3(const f32x4_t& a, const f32x4_t& b, f32x4_t acc) {
+    uint2 ah, al, bh, bl;
+    split_pair(a[0], a[1], ah.x, al.x);
+    split_pair(a[2], a[3], ah.y, al.y);
+    split_pair(b[0], b[1], bh.x, bl.x);
+    split_pair(b[2], b[3], bh.y, bl.y);
+    const s16x4_t ahf = __builtin_bit_cast(s16x4_t, ah), alf = __builtin_bit_cast(s16x4_t, al);
+    const s16x4_t bhf = __builtin_bit_cast(s16x4_t, bh), blf = __builtin_bit_cast(s16x4_t, bl);
+    acc = mma(ahf, bhf, acc);
+    acc = mma(ahf, blf, acc);
+    return mma(alf, bhf, acc);
+}
+
+template <int J>
+__device__ __forceinline__ void col_sweep(Smem& sm, int par, int m, int g) {
+    const float bcol = sm.bet[J][16 * J + m];
+    const f32x4_t djb = *reinterpret_cast<const f32x4_t*>(sm.dtr[J] + m * FB + 4 * g);
+    f32x4_t aop[NCT][NCT];    // A_{bi,kb}[m][4 g + s]
+    f32x4_t dop[NCT];         // -D_bi[m][4 g + s]
+#pragma unroll
+    for (int bi = J + 1; bi < NCT; ++bi) {
+#pragma unroll
+        for (int kb = J; kb < bi; ++kb) {
+            const float* ab = sm.at[bidx(bi, kb)];
+#pragma unroll
+            for (int s = 0; s < 4; ++s) aop[bi][kb][s] = ab[(4 * g + s) * FB + m];
+        }
+#pragma unroll
+        for (int s = 0; s < 4; ++s) dop[bi][s] = -sm.dtr[bi][(4 * g + s) * FB + m];
+    }
+    f32x4_t tz[NCT];
+#pragma unroll
+    for (int bi = J + 1; bi < NCT; ++bi) {
+        // one accumulator per term of the sum, added at the end
+        const f32x4_t zero = {0.f, 0.f, 0.f, 0.f};
+        f32x4_t yk[NCT];
+#pragma unroll
+        for (int kb = J; kb < bi; ++kb) yk[kb] = prod3(aop[bi][kb], kb == J ? djb : tz[kb], zero);
+        f32x4_t y = yk[J];
+#pragma unroll
+        for (int kb = J + 1; kb < bi; ++kb) y += yk[kb];
+        const f32x4_t z = prod3(dop[bi], y, zero);
+        tz[bi] = z;
+        const int ob = bidx(bi, J);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            split_bf16(z[i] * bcol, sm.th[par][ob][4 * g + i][m], sm.tl[par][ob][4 * g + i][m]);
+    }
+}
+
+// D = (I + N)^-1 for a strictly lower 16 x 16 block N (N^16 = 0), as the
+// product (I - N)(I + N^2)(I + N^4)(I + N^8) (the factors are polynomials in N
+// and commute), each product on three bf16 MFMAs (prod3).  An accumulator
+// holding X is the B operand of X and the A operand of X^T, so each power is
+// formed both ways and every product reads registers only.
+//   nat: A operand of N, N[m][4 g + s];  nb: B operand of N, N[4 g + s][m].
+// Returns D in accumulator layout.
+__device__ __forceinline__ f32x4_t block_inverse(const f32x4_t& nat, const f32x4_t& nb, int m, int g) {
+    auto prod = [](const f32x4_t& a, const f32x4_t& b, const f32x4_t& acc) { return prod3(a, b, acc); };
+    const f32x4_t zero = {0.f, 0.f, 0.f, 0.f};
+    const f32x4_t n2 = prod(nat, nb, zero);    // N^2
+    const f32x4_t n2t = prod(nb, nat, zero);   // (N^2)^T = N^T N^T
+    const f32x4_t n3 = prod(nat, n2, zero);    // N^3 = N N^2
+    const f32x4_t n4 = prod(n2t, n2, zero);    // N^4 = N^2 N^2
+    const f32x4_t n4t = prod(n2, n2t, zero);   // (N^4)^T
+    f32x4_t p1;                                // (I - N)(I + N^2) = I - N + N^2 - N^3
+#pragma unroll
+    for (int i = 0; i < 4; ++i) p1[i] = ((4 * g + i == m) ? 1.f : 0.f) - nb[i] + n2[i] - n3[i];
+    const f32x4_t p2 = prod(n4t, p1, p1);      // (I + N^4) P1
+    const f32x4_t n8t = prod(n4, n4t, zero);   // (N^8)^T
+    return prod(n8t, p2, p2);                  // (I + N^8) P2
 }
 
 // NS state waves (4 or 8), each owning D / NS value columns.
@@ -155,6 +257,21 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             const int par = c & 1;
             const int L = min(C, seq_len - c * C);
             const int t0 = seq_beg + c * C;
+            // K^T of chunk c (read only by the state update at the end of this
+            // iteration, after every state wave has written its part)
+            for (int i = tid; i < (C / 2) * SEGS; i += 64 * NS) {
+                const int p = i % (C / 2), seg = i / (C / 2);
+                const uint4 r0 = *reinterpret_cast<const uint4*>(&sm.kb[par][2 * p][seg * 8]);
+                const uint4 r1 = *reinterpret_cast<const uint4*>(&sm.kb[par][2 * p + 1][seg * 8]);
+                const uint32_t a[4] = {r0.x, r0.y, r0.z, r0.w};
+                const uint32_t b[4] = {r1.x, r1.y, r1.z, r1.w};
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    *reinterpret_cast<uint32_t*>(&sm.kt[seg * 8 + 2 * j][2 * p]) = (a[j] & 0xFFFFu) | (b[j] << 16);
+                    *reinterpret_cast<uint32_t*>(&sm.kt[seg * 8 + 2 * j + 1][2 * p]) = (a[j] >> 16) | (b[j] & 0xFFFF0000u);
+                }
+            }
+            signal(&sm.cnt[CNT_KT], lane);
             // K S0^T (S0 hi + lo) and Q S0^T (S0 hi)
             f32x4_t ks[NCT][NVT], qs[NCT][NVT];
 #pragma unroll
@@ -164,22 +281,33 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     ks[ct][vt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
                     qs[ct][vt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
                 }
+            bf16x8_t ak[2][NCT], aq[2][NCT];  // operands of two contraction steps in flight
 #pragma unroll
-            for (int kk = 0; kk < D; kk += 32) {
-                bf16x8_t bh[NVT], bl[NVT];
+            for (int ct = 0; ct < NCT; ++ct) {
+                ak[0][ct] = lds_frag_perm<32>(&sm.kb[par][16 * ct + m][0], 0, gq);
+                aq[0][ct] = lds_frag_perm<32>(&sm.qb[16 * ct + m][0], 0, gq);
+            }
 #pragma unroll
-                for (int vt = 0; vt < NVT; ++vt) acc_frag<32>(st[kk / 16][vt], st[kk / 16 + 1][vt], bh[vt], bl[vt]);
+            for (int kq = 0; kq < D / 32; ++kq) {
+                const int cur = kq & 1;
+                if (kq + 1 < D / 32) {
 #pragma unroll
-                for (int ct = 0; ct < NCT; ++ct) {
-                    const bf16x8_t ak = lds_frag_perm<32>(&sm.kb[par][16 * ct + m][0], kk, gq);
-                    const bf16x8_t aq = lds_frag_perm<32>(&sm.qb[16 * ct + m][0], kk, gq);
-#pragma unroll
-                    for (int vt = 0; vt < NVT; ++vt) {
-                        ks[ct][vt] = mma(ak, bh[vt], ks[ct][vt]);
-                        ks[ct][vt] = mma(ak, bl[vt], ks[ct][vt]);
-                        qs[ct][vt] = mma(aq, bh[vt], qs[ct][vt]);
+                    for (int ct = 0; ct < NCT; ++ct) {
+                        ak[cur ^ 1][ct] = lds_frag_perm<32>(&sm.kb[par][16 * ct + m][0], 32 * (kq + 1), gq);
+                        aq[cur ^ 1][ct] = lds_frag_perm<32>(&sm.qb[16 * ct + m][0], 32 * (kq + 1), gq);
                     }
                 }
+                bf16x8_t bh[NVT], bl[NVT];
+#pragma unroll
+                for (int vt = 0; vt < NVT; ++vt) acc_frag<32>(st[2 * kq][vt], st[2 * kq + 1][vt], bh[vt], bl[vt]);
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                    for (int vt = 0; vt < NVT; ++vt) {
+                        ks[ct][vt] = mma(ak[cur][ct], bh[vt], ks[ct][vt]);
+                        ks[ct][vt] = mma(ak[cur][ct], bl[vt], ks[ct][vt]);
+                        qs[ct][vt] = mma(aq[cur][ct], bh[vt], qs[ct][vt]);
+                    }
             }
             signal(&sm.cnt[CNT_QFREE], lane);
             // W = V - diag(exp(gamma)) K S0^T (in ks); O starts as diag(exp(gamma)) Q S0^T (in qs)
@@ -235,17 +363,30 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     for (int vt = 0; vt < NVT; ++vt) qs[ct][vt] = mma(ap, uh[vt], qs[ct][vt]);
                 }
             }
+            // Outputs: a 4 x 4 transpose inside each quad of lanes turns "4 rows of
+            // one column" into "4 columns of one row", stored as 8 bytes.
+            {
+                const int kq = m & 3;
+                const bool odd = (kq & 1) != 0, hi2 = (kq & 2) != 0;
 #pragma unroll
-            for (int ct = 0; ct < NCT; ++ct)
+                for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int row = 16 * ct + 4 * gq + i;
-                    if (row < L) {
-                        uint16_t* orow = o + (size_t)(t0 + row) * v_stride + (size_t)h * D + vcol0 + m;
-#pragma unroll
-                        for (int vt = 0; vt < NVT; ++vt) orow[16 * vt] = f32_to_bf16(scale * qs[ct][vt][i]);
+                    for (int vt = 0; vt < NVT; ++vt) {
+                        const f32x4_t a0 = qs[ct][vt] * scale;
+                        const float x0 = dpp<DPP_QUAD_XOR1>(a0[1]), x1 = dpp<DPP_QUAD_XOR1>(a0[0]);
+                        const float x2 = dpp<DPP_QUAD_XOR1>(a0[3]), x3 = dpp<DPP_QUAD_XOR1>(a0[2]);
+                        const f32x4_t a1 = {odd ? x0 : a0[0], odd ? a0[1] : x1, odd ? x2 : a0[2], odd ? a0[3] : x3};
+                        const float u0 = dpp<DPP_QUAD_XOR2>(a1[2]), u1 = dpp<DPP_QUAD_XOR2>(a1[3]);
+                        const float u2 = dpp<DPP_QUAD_XOR2>(a1[0]), u3 = dpp<DPP_QUAD_XOR2>(a1[1]);
+                        const f32x4_t a2 = {hi2 ? u0 : a1[0], hi2 ? u1 : a1[1], hi2 ? a1[2] : u2, hi2 ? a1[3] : u3};
+                        const int row = 16 * ct + 4 * gq + kq;
+                        if (row < L) {
+                            const uint2 pk = {cvt_pk(a2[0], a2[1]), cvt_pk(a2[2], a2[3])};
+                            *reinterpret_cast<uint2*>(o + (size_t)(t0 + row) * v_stride + (size_t)h * D + vcol0 +
+                                                      16 * vt + 4 * (m >> 2)) = pk;
+                        }
                     }
-                }
+            }
             // S^T = exp(gamma_last) S^T + K^T (diag(exp(gamma_last - gamma)) U)   (hi + lo)
             f32x4_t eglv[NCT];
 #pragma unroll
@@ -255,7 +396,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
                 for (int vt = 0; vt < NVT; ++vt) st[dt][vt] *= eg_last;
-            wait_ge(&sm.cnt[CNT_KT], (unsigned)(NP * (c + 1)));
+            wait_ge(&sm.cnt[CNT_KT], (unsigned)(NS * (c + 1)));
 #pragma unroll
             for (int kc = 0; kc < C; kc += 32) {
                 bf16x8_t uth[NVT], utl[NVT];
@@ -314,20 +455,6 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             rg = in ? g[(size_t)(tb + lane) * H_v + h] : 0.f;
             rb = in ? beta[(size_t)(tb + lane) * H_v + h] : 0.f;
         };
-        auto build_kt = [&](int par) {
-            for (int i = ptid; i < (C / 2) * SEGS; i += 64 * NP) {
-                const int p = i % (C / 2), seg = i / (C / 2);
-                const uint4 r0 = *reinterpret_cast<const uint4*>(&sm.kb[par][2 * p][seg * 8]);
-                const uint4 r1 = *reinterpret_cast<const uint4*>(&sm.kb[par][2 * p + 1][seg * 8]);
-                const uint32_t a[4] = {r0.x, r0.y, r0.z, r0.w};
-                const uint32_t b[4] = {r1.x, r1.y, r1.z, r1.w};
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    *reinterpret_cast<uint32_t*>(&sm.kt[seg * 8 + 2 * j][2 * p]) = (a[j] & 0xFFFFu) | (b[j] << 16);
-                    *reinterpret_cast<uint32_t*>(&sm.kt[seg * 8 + 2 * j + 1][2 * p]) = (a[j] >> 16) | (b[j] & 0xFFFF0000u);
-                }
-            }
-        };
         // Prepare every state-independent input of chunk x from the registers;
         // `free_target` is what the Q-free / V-free counters must reach before
         // the single Q and V buffers may be overwritten.
@@ -340,13 +467,8 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                 const int r = i / SEGS, seg = i - r * SEGS;
                 *reinterpret_cast<uint4*>(&sm.kb[par][r][seg * 8]) = rk[it];
             }
-            float gx = rg;
-#pragma unroll
-            for (int d = 1; d < 64; d <<= 1) {
-                const float y = __shfl_up(gx, d);
-                if (lane >= d) gx += y;
-            }
-            const float glast = __shfl(gx, C - 1);
+            const float gx = wave_prefix_sum(rg);
+            const float glast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gx), C - 1));
             sm.gam[pw][lane] = gx;
             sm.bet[pw][lane] = rb;
             if (pw == 0) {
@@ -354,93 +476,65 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                 sm.egl[par][lane] = fast_exp(glast - gx);
             }
             pbar();  // K of chunk x complete
-            // G = K K^T tiles -> A (fp32)
-            for (int tri = pw; tri < NBLK; tri += NP) {
-                int ti = 0;
-                while ((ti + 1) * (ti + 2) / 2 <= tri) ++ti;
-                const int tj = tri - ti * (ti + 1) / 2;
-                f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-                const uint16_t* arow = &sm.kb[par][16 * ti + m][0];
-                const uint16_t* brow = &sm.kb[par][16 * tj + m][0];
+            // G = K K^T tiles pw, pw + 4, pw + 8 -> A^T (fp32); all operand loads
+            // are issued before the products.
+            {
+                constexpr int NJ = 3;
+                bf16x8_t fa[NJ][D / 32], fb[NJ][D / 32];
 #pragma unroll
-                for (int kk = 0; kk < D; kk += 32)
-                    acc = mma(lds_frag_nat<32>(arow, kk, gq), lds_frag_nat<32>(brow, kk, gq), acc);
-                const int col = 16 * tj + m;
-                const float gcol = sm.gam[pw][col];
+                for (int jj = 0; jj < NJ; ++jj) {
+                    const int tri = min(pw + NP * jj, NBLK - 1);
+                    const int ti = tri_row(tri), tj = tri - ti * (ti + 1) / 2;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int row = 16 * ti + 4 * gq + i;
-                    const float dec = fast_exp(sm.gam[pw][row] - gcol);
-                    sm.a[tri][4 * gq + i][m] = col < row ? sm.bet[pw][row] * dec * acc[i] : 0.f;
+                    for (int kq = 0; kq < D / 32; ++kq) {
+                        fa[jj][kq] = lds_frag_nat<32>(&sm.kb[par][16 * ti + m][0], 32 * kq, gq);
+                        fb[jj][kq] = lds_frag_nat<32>(&sm.kb[par][16 * tj + m][0], 32 * kq, gq);
+                    }
+                }
+#pragma unroll
+                for (int jj = 0; jj < NJ; ++jj) {
+                    const int tri = pw + NP * jj;
+                    if (tri >= NBLK) break;
+                    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int kq = 0; kq < D / 32; ++kq) acc = mma(fa[jj][kq], fb[jj][kq], acc);
+                    const int ti = tri_row(tri), tj = tri - ti * (ti + 1) / 2;
+                    const int col = 16 * tj + m;
+                    const float gcol = sm.gam[pw][col];
+                    const f32x4_t grow = *reinterpret_cast<const f32x4_t*>(&sm.gam[pw][16 * ti + 4 * gq]);
+                    const f32x4_t brow = *reinterpret_cast<const f32x4_t*>(&sm.bet[pw][16 * ti + 4 * gq]);
+                    f32x4_t val;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int row = 16 * ti + 4 * gq + i;
+                        val[i] = col < row ? brow[i] * fast_exp(grow[i] - gcol) * acc[i] : 0.f;
+                    }
+                    *reinterpret_cast<f32x4_t*>(&sm.at[tri][m * FB + 4 * gq]) = val;
                 }
             }
             pbar();  // A complete
-            // T = (I + A)^-1.  Every producer wave inverts all four diagonal blocks
-            // at once (lane 16 b + m: column m of block b, forward substitution
-            // with each row sum split over two chains), writes T diag(beta) of
-            // block pw, and keeps the diagonal blocks its own sweep needs in a
-            // private LDS slot.  Wave j < 3 then forms the blocks below the
-            // diagonal of block column j one after another,
-            //     T_bj = -D_b sum_{kb=j}^{b-1} A_{b,kb} T_{kb,j},   T_jj = D_j,
-            // keeping each result in its accumulator (as a B operand it supplies
-            // contraction row 4 gq + s at step s).  A is complete and each wave
-            // reads only its own slots, so no producer barrier is needed here.
+            // T = (I + A)^-1.  Wave pw inverts diagonal block pw on the matrix
+            // cores, writes its T diag(beta) and shares D^T with the other
+            // producers; after one producer barrier, wave j < 3 sweeps block
+            // column j below the diagonal.
             {
-                const int b = lane >> 4;
-                const int bb = bidx(b, b);
-                float xs[16];
+                const int bb = bidx(pw, pw);
+                const float* atb = sm.at[bb];
+                const f32x4_t nat = {atb[(4 * gq) * FB + m], atb[(4 * gq + 1) * FB + m],
+                                     atb[(4 * gq + 2) * FB + m], atb[(4 * gq + 3) * FB + m]};
+                const f32x4_t nb = *reinterpret_cast<const f32x4_t*>(atb + m * FB + 4 * gq);
+                const f32x4_t dacc = block_inverse(nat, nb, m, gq);
+                const float bcol = sm.bet[pw][16 * pw + m];
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    float a0 = (r == m) ? 1.f : 0.f, a1 = 0.f;
-#pragma unroll
-                    for (int i = 0; i < r; ++i) {
-                        if (i & 1) a1 = fmaf(-sm.a[bb][r][i], xs[i], a1);
-                        else a0 = fmaf(-sm.a[bb][r][i], xs[i], a0);
-                    }
-                    xs[r] = a0 + a1;
-                }
-                if (b == pw) {
-                    const float bcol = sm.bet[pw][16 * b + m];
-#pragma unroll
-                    for (int r = 0; r < 16; ++r)
-                        split_bf16(xs[r] * bcol, sm.th[par][bb][r][m], sm.tl[par][bb][r][m]);
-                }
-                if (pw < NCT - 1 && b >= pw) {
-                    float (*slot)[FP] = sm.t[dslot(pw, b)];
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) slot[r][m] = xs[r];
-                }
+                for (int i = 0; i < 4; ++i)
+                    split_bf16(dacc[i] * bcol, sm.th[par][bb][4 * gq + i][m], sm.tl[par][bb][4 * gq + i][m]);
+                *reinterpret_cast<f32x4_t*>(sm.dtr[pw] + m * FB + 4 * gq) = dacc;
             }
-            if (pw < NCT - 1) {
-                const int j = pw;
-                const float bcol = sm.bet[pw][16 * j + m];
-                const float (*dj)[FP] = sm.t[dslot(j, j)];
-                f32x4_t tz[NCT];
-#pragma unroll
-                for (int bi = 1; bi < NCT; ++bi) {
-                    tz[bi] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-                    if (bi <= j) continue;
-                    f32x4_t y = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int s = 0; s < 4; ++s)
-                        y = mma_f32(sm.a[bidx(bi, j)][m][4 * gq + s], dj[4 * gq + s][m], y);
-#pragma unroll
-                    for (int kb = 1; kb < bi; ++kb) {
-                        if (kb <= j) continue;
-#pragma unroll
-                        for (int s = 0; s < 4; ++s) y = mma_f32(sm.a[bidx(bi, kb)][m][4 * gq + s], tz[kb][s], y);
-                    }
-                    const float (*db)[FP] = sm.t[dslot(j, bi)];
-                    f32x4_t z = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int s = 0; s < 4; ++s) z = mma_f32(-db[m][4 * gq + s], y[s], z);
-                    tz[bi] = z;
-                    const int ob = bidx(bi, j);
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        split_bf16(z[i] * bcol, sm.th[par][ob][4 * gq + i][m], sm.tl[par][ob][4 * gq + i][m]);
-                }
-            }
+            pbar();  // diagonal blocks of T complete
+            // Block column sweep of wave pw < 3 (below the diagonal of T).
+            if (pw == 0) col_sweep<0>(sm, par, m, gq);
+            else if (pw == 1) col_sweep<1>(sm, par, m, gq);
+            else if (pw == 2) col_sweep<2>(sm, par, m, gq);
             // stage Q and V once the state waves are done with the previous chunk's
             wait_ge(&sm.cnt[CNT_QFREE], free_target);
 #pragma unroll
@@ -457,24 +551,36 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                 *reinterpret_cast<uint4*>(&sm.vb[r][seg * 8]) = rv[it];
             }
             pbar();  // Q of chunk x complete
-            // P = Q K^T tiles -> masked scores (bf16)
-            for (int tri = pw; tri < NBLK; tri += NP) {
-                int ti = 0;
-                while ((ti + 1) * (ti + 2) / 2 <= tri) ++ti;
-                const int tj = tri - ti * (ti + 1) / 2;
-                f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-                const uint16_t* arow = &sm.qb[16 * ti + m][0];
-                const uint16_t* brow = &sm.kb[par][16 * tj + m][0];
+            // P = Q K^T tiles -> masked scores (bf16); operands loaded first
+            {
+                constexpr int NJ = 3;
+                bf16x8_t fa[NJ][D / 32], fb[NJ][D / 32];
 #pragma unroll
-                for (int kk = 0; kk < D; kk += 32)
-                    acc = mma(lds_frag_nat<32>(arow, kk, gq), lds_frag_nat<32>(brow, kk, gq), acc);
-                const int col = 16 * tj + m;
-                const float gcol = sm.gam[pw][col];
+                for (int jj = 0; jj < NJ; ++jj) {
+                    const int tri = min(pw + NP * jj, NBLK - 1);
+                    const int ti = tri_row(tri), tj = tri - ti * (ti + 1) / 2;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int row = 16 * ti + 4 * gq + i;
-                    const float dec = fast_exp(sm.gam[pw][row] - gcol);
-                    sm.pm[par][tri][4 * gq + i][m] = f32_to_bf16(col <= row ? dec * acc[i] : 0.f);
+                    for (int kq = 0; kq < D / 32; ++kq) {
+                        fa[jj][kq] = lds_frag_nat<32>(&sm.qb[16 * ti + m][0], 32 * kq, gq);
+                        fb[jj][kq] = lds_frag_nat<32>(&sm.kb[par][16 * tj + m][0], 32 * kq, gq);
+                    }
+                }
+#pragma unroll
+                for (int jj = 0; jj < NJ; ++jj) {
+                    const int tri = pw + NP * jj;
+                    if (tri >= NBLK) break;
+                    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int kq = 0; kq < D / 32; ++kq) acc = mma(fa[jj][kq], fb[jj][kq], acc);
+                    const int ti = tri_row(tri), tj = tri - ti * (ti + 1) / 2;
+                    const int col = 16 * tj + m;
+                    const float gcol = sm.gam[pw][col];
+                    const f32x4_t grow = *reinterpret_cast<const f32x4_t*>(&sm.gam[pw][16 * ti + 4 * gq]);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int row = 16 * ti + 4 * gq + i;
+                        sm.pm[par][tri][4 * gq + i][m] = f32_to_bf16(col <= row ? fast_exp(grow[i] - gcol) * acc[i] : 0.f);
+                    }
                 }
             }
         };
@@ -486,8 +592,6 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
         }
         __syncthreads();  // chunk 0 prepared
         for (int c = 0; c < nch; ++c) {
-            build_kt(c & 1);
-            signal(&sm.cnt[CNT_KT], lane);
             if (c + 1 < nch) {
                 prepare(c + 1, (unsigned)(NS * (c + 1)));
                 if (c + 2 < nch) load_chunk(c + 2);
