@@ -16,13 +16,15 @@
 //     own (block inverses, block column sweep and masked scores all stay in
 //     registers), writes them to its result slot once the state waves are done
 //     with the slot's previous chunk, and finally stages the chunk's K, Q, V
-//     rows into the single LDS row buffers once the state waves have finished
-//     reading the previous chunk's.  A producer therefore has about four state
-//     iterations to prepare a chunk, and none of its latency is on the state
-//     waves' path.
+//     rows into LDS (K double-buffered by chunk parity, Q and V single) once
+//     the state waves have released the buffers.  A producer therefore has
+//     about four state iterations to prepare a chunk, and none of its latency
+//     is on the state waves' path.
 //
-// Waves meet only through counters in LDS (chunks staged, buffers released,
-// slot results ready, slots released, K^T parts written).  Every wait is a
+// Operands that run along a column of a row-major LDS array (K^T for the state
+// update, V for W) come from the gfx950 transpose read, so no transposed copy
+// is ever built.  Waves meet only through counters in LDS (chunks staged,
+// buffers released, slot results ready, slots released).  Every wait is a
 // bounded spin; LDS operations of a wave execute in order, so a counter
 // increment issued after a wave's LDS stores (or reads) is observed only after
 // those have executed.
@@ -36,7 +38,6 @@ constexpr int D = 128, C = 64;
 constexpr int NP = 4;                 // producer waves = result slots
 constexpr int NDT = D / 16, NCT = C / 16;
 constexpr int PD = D + 8;             // LDS pitch (bf16) of [C][D] arrays
-constexpr int PC = C + 8;             // LDS pitch (bf16) of [D][C] arrays
 constexpr int NBLK = NCT * (NCT + 1) / 2;   // lower-triangular 16 x 16 blocks (10)
 constexpr int SEGS = D / 8;                 // 16-byte segments per q/k/v row
 constexpr int SITEMS = C * SEGS / 64;       // staged segments per producer lane (16)
@@ -56,19 +57,18 @@ struct Slot {
 enum {
     CNT_STG_KQ = 0,   // chunks whose K and Q rows are staged
     CNT_STG_V,        // chunks whose V rows are staged
-    CNT_KQFREE,       // state-wave releases of the K and Q row buffers
+    CNT_KFREE,        // state-wave releases of a K row buffer (after the update)
+    CNT_QFREE,        // state-wave releases of the Q row buffer
     CNT_VFREE,        // state-wave releases of the V row buffer
-    CNT_KT,           // K^T parts written (NS per chunk)
     CNT_READY0,       // + p: chunks written to slot p
     CNT_SFREE0 = CNT_READY0 + NP,  // + p: state-wave releases of slot p
     NCNT = CNT_SFREE0 + NP
 };
 
 struct Smem {
-    uint16_t kb[C][PD];               // K rows of the chunk the state waves work on
-    uint16_t qb[C][PD];               // Q rows
+    uint16_t kb[2][C][PD];            // K rows, by chunk parity
+    uint16_t qb[C][PD];               // Q rows of the chunk the state waves work on
     uint16_t vb[C][PD];               // V rows
-    uint16_t kt[2][D][PC];            // K^T, by chunk parity
     Slot slot[NP];
     alignas(16) float gam[NP][C];     // per producer: gate prefix of its chunk
     alignas(16) float bet[NP][C];     // per producer: beta of its chunk
@@ -119,6 +119,28 @@ __device__ __forceinline__ bf16x8_t blk_frag(const uint16_t (*blocks)[16][16], c
     const uint16_t* p1 = (j0 + 1 <= ct) ? &blocks[bidx(ct, j0 + 1)][m][4 * g] : &zero[m][4 * g];
     const uint2 lo = *reinterpret_cast<const uint2*>(p0);
     const uint2 hi = *reinterpret_cast<const uint2*>(p1);
+    uint4 u = {lo.x, lo.y, hi.x, hi.y};
+    return __builtin_bit_cast(bf16x8_t, u);
+}
+
+typedef short tr16x4_t __attribute__((ext_vector_type(4)));
+
+// gfx950 transpose read (ds_read_b64_tr_b16): within each group of 16 lanes,
+// lane i receives element i % 4 of the 8-byte words addressed by lanes
+// i / 4 + 4 e, e = 0..3.  With lane l addressing row r0 + l / 4, column
+// c0 + 4 (l % 4) of a row-major array, lane i therefore gets rows r0..r0+3 of
+// column c0 + i.
+__device__ __forceinline__ uint2 lds_tr4(const uint16_t* p) {
+    const tr16x4_t r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) tr16x4_t*)p);
+    return __builtin_bit_cast(uint2, r);
+}
+
+// A operand whose rows are columns c0..c0+15 of a row-major [row][col] bf16
+// array, contraction over rows r0..r0+31 in the permuted order (slot j < 4:
+// row r0 + 4 g + j; slot j >= 4: row r0 + 16 + 4 g + (j - 4)).
+__device__ __forceinline__ bf16x8_t lds_frag_tr(const uint16_t (*a)[PD], int r0, int c0, int m, int g) {
+    const uint2 lo = lds_tr4(&a[r0 + 4 * g + (m >> 2)][c0 + 4 * (m & 3)]);
+    const uint2 hi = lds_tr4(&a[r0 + 16 + 4 * g + (m >> 2)][c0 + 4 * (m & 3)]);
     uint4 u = {lo.x, lo.y, hi.x, hi.y};
     return __builtin_bit_cast(bf16x8_t, u);
 }
@@ -233,22 +255,8 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             const int L = min(C, seq_len - c * C);
             const int t0 = seq_beg + c * C;
             const Slot& sl = sm.slot[c % NP];
+            const uint16_t (*kb)[PD] = sm.kb[par];
             wait_ge(&sm.cnt[CNT_STG_KQ], (unsigned)(c + 1));
-            // K^T of chunk c (read only by the state update at the end of this
-            // iteration, after every state wave has written its part)
-            for (int i = tid; i < (C / 2) * SEGS; i += 64 * NS) {
-                const int p = i % (C / 2), seg = i / (C / 2);
-                const uint4 r0 = *reinterpret_cast<const uint4*>(&sm.kb[2 * p][seg * 8]);
-                const uint4 r1 = *reinterpret_cast<const uint4*>(&sm.kb[2 * p + 1][seg * 8]);
-                const uint32_t a[4] = {r0.x, r0.y, r0.z, r0.w};
-                const uint32_t b[4] = {r1.x, r1.y, r1.z, r1.w};
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    *reinterpret_cast<uint32_t*>(&sm.kt[par][seg * 8 + 2 * j][2 * p]) = (a[j] & 0xFFFFu) | (b[j] << 16);
-                    *reinterpret_cast<uint32_t*>(&sm.kt[par][seg * 8 + 2 * j + 1][2 * p]) = (a[j] >> 16) | (b[j] & 0xFFFF0000u);
-                }
-            }
-            signal(&sm.cnt[CNT_KT], lane);
             // K S0^T (S0 hi + lo), rows t; (Q S0^T)^T (S0 hi), rows v
             f32x4_t ks[NCT][NVT], ot[NVT][NCT];
 #pragma unroll
@@ -261,7 +269,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             bf16x8_t ak[2][NCT], aq[2][NCT];  // operands of two contraction steps in flight
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) {
-                ak[0][ct] = lds_frag_perm<32>(&sm.kb[16 * ct + m][0], 0, gq);
+                ak[0][ct] = lds_frag_perm<32>(&kb[16 * ct + m][0], 0, gq);
                 aq[0][ct] = lds_frag_perm<32>(&sm.qb[16 * ct + m][0], 0, gq);
             }
 #pragma unroll
@@ -270,7 +278,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                 if (kq + 1 < D / 32) {
 #pragma unroll
                     for (int ct = 0; ct < NCT; ++ct) {
-                        ak[cur ^ 1][ct] = lds_frag_perm<32>(&sm.kb[16 * ct + m][0], 32 * (kq + 1), gq);
+                        ak[cur ^ 1][ct] = lds_frag_perm<32>(&kb[16 * ct + m][0], 32 * (kq + 1), gq);
                         aq[cur ^ 1][ct] = lds_frag_perm<32>(&sm.qb[16 * ct + m][0], 32 * (kq + 1), gq);
                     }
                 }
@@ -286,7 +294,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                         ot[vt][ct] = mma(bh[vt], aq[cur][ct], ot[vt][ct]);
                     }
             }
-            signal(&sm.cnt[CNT_KQFREE], lane);
+            signal(&sm.cnt[CNT_QFREE], lane);
             // W = V - diag(exp(gamma)) K S0^T (in ks)
             wait_ge(&sm.cnt[CNT_READY0 + c % NP], (unsigned)(c / NP + 1));
             wait_ge(&sm.cnt[CNT_STG_V], (unsigned)(c + 1));
@@ -296,12 +304,14 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-                for (int vt = 0; vt < NVT; ++vt)
+                for (int vt = 0; vt < NVT; ++vt) {
+                    // V[16 ct + 4 gq + i][vcol0 + 16 vt + m], i = 0..3
+                    const uint2 vv = lds_tr4(&sm.vb[16 * ct + 4 * gq + (m >> 2)][vcol0 + 16 * vt + 4 * (m & 3)]);
+                    const float vf[4] = {bf16_to_f32(vv.x & 0xFFFFu), bf16_to_f32(vv.x >> 16),
+                                         bf16_to_f32(vv.y & 0xFFFFu), bf16_to_f32(vv.y >> 16)};
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const float vv = bf16_to_f32(sm.vb[16 * ct + 4 * gq + i][vcol0 + 16 * vt + m]);
-                        ks[ct][vt][i] = fmaf(-egr[ct][i], ks[ct][vt][i], vv);
-                    }
+                    for (int i = 0; i < 4; ++i) ks[ct][vt][i] = fmaf(-egr[ct][i], ks[ct][vt][i], vf[i]);
+                }
             signal(&sm.cnt[CNT_VFREE], lane);
             // U = T diag(beta) W  (hi*hi + hi*lo + lo*hi)
             f32x4_t uu[NCT][NVT];
@@ -371,7 +381,6 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
                 for (int vt = 0; vt < NVT; ++vt) st[dt][vt] *= eg_last;
-            wait_ge(&sm.cnt[CNT_KT], (unsigned)(NS * (c + 1)));
 #pragma unroll
             for (int kc = 0; kc < C; kc += 32) {
                 bf16x8_t uth[NVT], utl[NVT];
@@ -380,7 +389,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     acc_frag<32>(uu[kc / 16][vt] * eglv[kc / 16], uu[kc / 16 + 1][vt] * eglv[kc / 16 + 1], uth[vt], utl[vt]);
 #pragma unroll
                 for (int dt = 0; dt < NDT; ++dt) {
-                    const bf16x8_t a = lds_frag_perm<32>(&sm.kt[par][16 * dt + m][0], kc, gq);
+                    const bf16x8_t a = lds_frag_tr(kb, kc, 16 * dt, m, gq);
 #pragma unroll
                     for (int vt = 0; vt < NVT; ++vt) {
                         st[dt][vt] = mma(a, uth[vt], st[dt][vt]);
@@ -388,6 +397,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     }
                 }
             }
+            signal(&sm.cnt[CNT_KFREE], lane);
         }
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt)
@@ -527,12 +537,13 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     sv[it] = *reinterpret_cast<const uint4*>(v + (size_t)(tb + r) * v_stride + (size_t)h * D + m * 8);
                 }
             }
-            wait_ge(&sm.cnt[CNT_KQFREE], (unsigned)(NS * x));
+            // K buffer x & 1 was last read by the update of chunk x - 2
+            wait_ge(&sm.cnt[CNT_KFREE], (unsigned)(x >= 2 ? NS * (x - 1) : 0));
 #pragma unroll
-            for (int it = 0; it < SITEMS; ++it) {
-                *reinterpret_cast<uint4*>(&sm.kb[4 * it + gq][m * 8]) = sk[it];
-                *reinterpret_cast<uint4*>(&sm.qb[4 * it + gq][m * 8]) = sq[it];
-            }
+            for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.kb[x & 1][4 * it + gq][m * 8]) = sk[it];
+            wait_ge(&sm.cnt[CNT_QFREE], (unsigned)(NS * x));
+#pragma unroll
+            for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.qb[4 * it + gq][m * 8]) = sq[it];
             signal(&sm.cnt[CNT_STG_KQ], lane);
             wait_ge(&sm.cnt[CNT_VFREE], (unsigned)(NS * x));
 #pragma unroll
