@@ -47,7 +47,7 @@ __device__ __forceinline__ constexpr int bidx(int i, int j) { return i * (i + 1)
 
 // Results of the state-independent part of one chunk.
 struct Slot {
-    uint16_t th[NBLK][16][16];   // T diag(beta) by lower blocks [row][col], bf16 hi
+    uint16_t th[NBLK][16][16];   // T diag(beta) by lower blocks, transposed [col][row], bf16 hi
     uint16_t tl[NBLK][16][16];   // bf16 lo
     uint16_t pm[NBLK][16][16];   // (M o Q K^T) by lower blocks [row t][col s], bf16
     alignas(16) float eg[C];     // exp(gamma)
@@ -145,6 +145,19 @@ __device__ __forceinline__ bf16x8_t lds_frag_tr(const uint16_t (*a)[PD], int r0,
     return __builtin_bit_cast(bf16x8_t, u);
 }
 
+// A operand from a stored lower-triangular block matrix kept transposed
+// ([col][row] per block): block row ct, contraction columns kc..kc+31 in the
+// permuted order; blocks above the diagonal read the zero block.
+__device__ __forceinline__ bf16x8_t blk_frag_t(const uint16_t (*blocks)[16][16], const uint16_t (*zero)[16],
+                                               int ct, int kc, int m, int g) {
+    const int j0 = kc >> 4;
+    const int r = 4 * g + (m >> 2), cc = 4 * (m & 3);
+    const uint2 lo = lds_tr4(&blocks[bidx(ct, j0)][r][cc]);
+    const uint2 hi = lds_tr4((j0 + 1 <= ct) ? &blocks[bidx(ct, j0 + 1)][r][cc] : &zero[r][cc]);
+    uint4 u = {lo.x, lo.y, hi.x, hi.y};
+    return __builtin_bit_cast(bf16x8_t, u);
+}
+
 // In the 16 x 16 block products below an accumulator holding X (lane m + 16 g,
 // element i = X[4 g + i][m]) is the B operand of X and the A operand of X^T
 // (contraction index 4 g + i), so prod(acc(X), acc(Y)) = acc(X^T Y).
@@ -193,11 +206,15 @@ __device__ __forceinline__ f32x4_t block_inverse(const f32x4_t& nat, const f32x4
 
 __device__ __forceinline__ bf16x8_t as_frag(const uint4& u) { return __builtin_bit_cast(bf16x8_t, u); }
 
-// Write x * scale as bf16 hi / lo into element [4 g + i][m] of a stored block.
-__device__ __forceinline__ void store_split(uint16_t (*th)[16], uint16_t (*tl)[16], const f32x4_t& x,
-                                            float scale, int m, int g) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) split_bf16(x[i] * scale, th[4 * g + i][m], tl[4 * g + i][m]);
+// Block X in accumulator layout, times scale, stored transposed as bf16 hi / lo:
+// element [m][4 g + i] of the stored block is X[4 g + i][m].
+__device__ __forceinline__ void store_split_t(uint16_t (*th)[16], uint16_t (*tl)[16], const f32x4_t& x,
+                                              float scale, int m, int g) {
+    uint2 hi, lo;
+    split_pair(x[0] * scale, x[1] * scale, hi.x, lo.x);
+    split_pair(x[2] * scale, x[3] * scale, hi.y, lo.y);
+    *reinterpret_cast<uint2*>(&th[m][4 * g]) = hi;
+    *reinterpret_cast<uint2*>(&tl[m][4 * g]) = lo;
 }
 
 // NS state waves (4 or 8), each owning D / NS value columns.
@@ -229,8 +246,26 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
     const size_t v_stride = (size_t)H_v * D;
     const size_t state_off = ((size_t)n * H_v + h) * D * D;
 
-    if (tid < NCNT) sm.cnt[tid] = 0;
+    // Every wave stages chunk 0's K, Q, V rows before the roles split, so the
+    // state waves can start on it while producer 0 prepares the rest.
+    if (tid < NCNT) sm.cnt[tid] = (tid == CNT_STG_KQ || tid == CNT_STG_V) && nch > 0 ? 1u : 0u;
     for (int i = tid; i < 16 * 16; i += 64 * (NS + NP)) (&sm.zero[0][0])[i] = 0;
+    if (nch > 0) {
+        const int L0 = min(C, seq_len);
+        for (int i = tid; i < C * SEGS; i += 64 * (NS + NP)) {
+            const int r = i / SEGS, seg = i - r * SEGS;
+            uint4 rk = {0, 0, 0, 0}, rq = {0, 0, 0, 0}, rv = {0, 0, 0, 0};
+            if (r < L0) {
+                const size_t tq = (size_t)(seq_beg + r) * qk_stride + (size_t)hq * D + seg * 8;
+                rk = *reinterpret_cast<const uint4*>(k + tq);
+                rq = *reinterpret_cast<const uint4*>(q + tq);
+                rv = *reinterpret_cast<const uint4*>(v + (size_t)(seq_beg + r) * v_stride + (size_t)h * D + seg * 8);
+            }
+            *reinterpret_cast<uint4*>(&sm.kb[0][r][seg * 8]) = rk;
+            *reinterpret_cast<uint4*>(&sm.qb[r][seg * 8]) = rq;
+            *reinterpret_cast<uint4*>(&sm.vb[r][seg * 8]) = rv;
+        }
+    }
     __syncthreads();
 
     if (wave < NS) {
@@ -327,8 +362,8 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) {
                     if (kc > 16 * ct + 15) continue;
-                    const bf16x8_t ah = blk_frag(sl.th, sm.zero, ct, kc, m, gq);
-                    const bf16x8_t al = blk_frag(sl.tl, sm.zero, ct, kc, m, gq);
+                    const bf16x8_t ah = blk_frag_t(sl.th, sm.zero, ct, kc, m, gq);
+                    const bf16x8_t al = blk_frag_t(sl.tl, sm.zero, ct, kc, m, gq);
 #pragma unroll
                     for (int vt = 0; vt < NVT; ++vt) {
                         uu[ct][vt] = mma(ah, wh[vt], uu[ct][vt]);
@@ -516,15 +551,17 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     *reinterpret_cast<uint2*>(&sl.pm[bidx(b, jt)][m][4 * gq]) = pk[bidx(b, jt)];
 #pragma unroll
             for (int b = 0; b < NCT; ++b) {
-                store_split(sl.th[bidx(b, b)], sl.tl[bidx(b, b)], dd[b], br[b], m, gq);
+                store_split_t(sl.th[bidx(b, b)], sl.tl[bidx(b, b)], dd[b], br[b], m, gq);
 #pragma unroll
-                for (int J = 0; J < b; ++J) store_split(sl.th[bidx(b, J)], sl.tl[bidx(b, J)], tt[bidx(b, J)], br[J], m, gq);
+                for (int J = 0; J < b; ++J) store_split_t(sl.th[bidx(b, J)], sl.tl[bidx(b, J)], tt[bidx(b, J)], br[J], m, gq);
             }
             sl.eg[lane] = fast_exp(gx);
             sl.egl[lane] = fast_exp(glast - gx);
             signal(&sm.cnt[CNT_READY0 + pw], lane);
             // ---- stage the chunk's K, Q, V rows once the state waves have
-            //      released the previous chunk's (row 4 it + gq, segment m)
+            //      released the previous chunk's (row 4 it + gq, segment m);
+            //      chunk 0 was staged by the whole workgroup
+            if (x == 0) continue;
             uint4 sk[SITEMS], sq[SITEMS], sv[SITEMS];
 #pragma unroll
             for (int it = 0; it < SITEMS; ++it) {
