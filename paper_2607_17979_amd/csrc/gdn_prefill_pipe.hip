@@ -41,6 +41,7 @@ constexpr int PD = D + 8;             // LDS pitch (bf16) of [C][D] arrays
 constexpr int NBLK = NCT * (NCT + 1) / 2;   // lower-triangular 16 x 16 blocks (10)
 constexpr int SEGS = D / 8;                 // 16-byte segments per q/k/v row
 constexpr int SITEMS = C * SEGS / 64;       // staged segments per producer lane (16)
+constexpr int SP = 20;                      // row pitch (fp32) of the producers' 16 x 16 scratch blocks
 constexpr int kSpinLimit = 1 << 20;
 
 __device__ __forceinline__ constexpr int bidx(int i, int j) { return i * (i + 1) / 2 + j; }
@@ -70,6 +71,7 @@ struct Smem {
     uint16_t qb[C][PD];               // Q rows of the chunk the state waves work on
     uint16_t vb[C][PD];               // V rows
     Slot slot[NP];
+    alignas(16) float scr[NP][NCT * 16 * SP];  // per producer: diagonal blocks of A, then of T
     alignas(16) float gam[NP][C];     // per producer: gate prefix of its chunk
     alignas(16) float bet[NP][C];     // per producer: beta of its chunk
     uint16_t zero[16][16];            // stands in for blocks above the diagonal
@@ -175,33 +177,6 @@ __device__ __forceinline__ f32x4_t prod3(const f32x4_t& a, const f32x4_t& b, f32
     acc = mma(ahf, bhf, acc);
     acc = mma(ahf, blf, acc);
     return mma(alf, bhf, acc);
-}
-
-// acc(X) -> acc(X^T), exactly: X^T I on fp32 MFMA.
-__device__ __forceinline__ f32x4_t transpose16(const f32x4_t& x, int m, int g) {
-    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < 4; ++s) acc = mma_f32(x[s], (4 * g + s == m) ? 1.f : 0.f, acc);
-    return acc;
-}
-
-// D = (I + N)^-1 for a strictly lower 16 x 16 block N (N^16 = 0), as the
-// product (I - N)(I + N^2)(I + N^4)(I + N^8) (the factors are polynomials in N
-// and commute), each power formed both ways so that every product reads
-// registers only.  nat = acc(N^T), nb = acc(N); returns acc(D).
-__device__ __forceinline__ f32x4_t block_inverse(const f32x4_t& nat, const f32x4_t& nb, int m, int g) {
-    const f32x4_t zero = {0.f, 0.f, 0.f, 0.f};
-    const f32x4_t n2 = prod3(nat, nb, zero);    // N^2
-    const f32x4_t n2t = prod3(nb, nat, zero);   // (N^2)^T
-    const f32x4_t n3 = prod3(nat, n2, zero);    // N^3
-    const f32x4_t n4 = prod3(n2t, n2, zero);    // N^4
-    const f32x4_t n4t = prod3(n2, n2t, zero);   // (N^4)^T
-    f32x4_t p1;                                 // (I - N)(I + N^2) = I - N + N^2 - N^3
-#pragma unroll
-    for (int i = 0; i < 4; ++i) p1[i] = ((4 * g + i == m) ? 1.f : 0.f) - nb[i] + n2[i] - n3[i];
-    const f32x4_t p2 = prod3(n4t, p1, p1);      // (I + N^4) P1
-    const f32x4_t n8t = prod3(n4, n4t, zero);   // (N^8)^T
-    return prod3(n8t, p2, p2);                  // (I + N^8) P2
 }
 
 __device__ __forceinline__ bf16x8_t as_frag(const uint4& u) { return __builtin_bit_cast(bf16x8_t, u); }
@@ -446,6 +421,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
         // ======================= producer waves ================================
         const int pw = wave - NS;
         Slot& sl = sm.slot[pw];
+        float* scr = sm.scr[pw];
         float* gam = sm.gam[pw];
         float* bet = sm.bet[pw];
         for (int x = pw, j = 0; x < nch; x += NP, ++j) {
@@ -522,13 +498,46 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     for (int i = 0; i < 4; ++i) at[bidx(b, kb)][i] = br[b] * fast_exp(gr[b] - gk[i]) * ag[i];
                 }
             }
-            // ---- T = (I + A)^-1: diagonal blocks D_b, then block columns
-            //      T_bJ = -D_b sum_{kb=J}^{b-1} A_{b,kb} T_{kb,J} (b > J).
+            // ---- T = (I + A)^-1: diagonal blocks D_b = (I + N_b)^-1 by forward
+            //      substitution in fp32, lane 16 b + j solving column j of
+            //      block b (rows of N_b are read as LDS broadcasts); then block
+            //      columns T_bJ = -D_b sum_{kb=J}^{b-1} A_{b,kb} T_{kb,J} (b > J).
+            float* scb = scr + gq * 16 * SP;  // this lane's block b = gq
+#pragma unroll
+            for (int b = 0; b < NCT; ++b)     // row m of N_b, columns 4 gq .. 4 gq + 3
+                *reinterpret_cast<f32x4_t*>(&scr[(16 * b + m) * SP + 4 * gq]) = nt[b];
+            // Row r + 1 of N_b is read while row r is solved; the scheduling
+            // fences keep the reads from being hoisted all at once.
+            float xs[16];
+            f32x4_t nrow[2][4];
+            xs[0] = (m == 0) ? 1.f : 0.f;
+            nrow[1][0] = *reinterpret_cast<const f32x4_t*>(&scb[1 * SP]);
+#pragma unroll
+            for (int r = 1; r < 16; ++r) {
+                const int cur = r & 1;
+                if (r + 1 < 16) {
+#pragma unroll
+                    for (int i4 = 0; i4 < r + 1; i4 += 4)
+                        nrow[cur ^ 1][i4 / 4] = *reinterpret_cast<const f32x4_t*>(&scb[(r + 1) * SP + i4]);
+                }
+                float acc = (r == m) ? 1.f : 0.f;
+#pragma unroll
+                for (int i = 0; i < r; ++i) acc = fmaf(-nrow[cur][i / 4][i % 4], xs[i], acc);
+                xs[r] = acc;
+                __builtin_amdgcn_sched_barrier(0);
+            }
+#pragma unroll
+            for (int r4 = 0; r4 < 16; r4 += 4)  // row m of the scratch block = column m of D_b
+                *reinterpret_cast<f32x4_t*>(&scb[m * SP + r4]) = f32x4_t{xs[r4], xs[r4 + 1], xs[r4 + 2], xs[r4 + 3]};
             f32x4_t dd[NCT], ddt[NCT], tt[NBLK];
 #pragma unroll
-            for (int b = 0; b < NCT; ++b) dd[b] = block_inverse(nt[b], nn[b], m, gq);
+            for (int b = 0; b < NCT; ++b) {     // acc(D_b): D_b[4 gq + i][m]
+                dd[b] = *reinterpret_cast<const f32x4_t*>(&scr[(16 * b + m) * SP + 4 * gq]);
+                if (b > 0) {                    // -acc(D_b^T): -D_b[m][4 gq + i]
 #pragma unroll
-            for (int b = 1; b < NCT; ++b) ddt[b] = -transpose16(dd[b], m, gq);
+                    for (int i = 0; i < 4; ++i) ddt[b][i] = -scr[(16 * b + 4 * gq + i) * SP + m];
+                }
+            }
             {
                 const f32x4_t zero4 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -562,16 +571,15 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             //      released the previous chunk's (row 4 it + gq, segment m);
             //      chunk 0 was staged by the whole workgroup
             if (x == 0) continue;
-            uint4 sk[SITEMS], sq[SITEMS], sv[SITEMS];
+            uint4 sk[SITEMS], sq[SITEMS];
 #pragma unroll
             for (int it = 0; it < SITEMS; ++it) {
                 const int r = 4 * it + gq;
-                sk[it] = sq[it] = sv[it] = uint4{0, 0, 0, 0};
+                sk[it] = sq[it] = uint4{0, 0, 0, 0};
                 if (r < L) {
                     const size_t tq = (size_t)(tb + r) * qk_stride + (size_t)hq * D + m * 8;
                     sk[it] = *reinterpret_cast<const uint4*>(k + tq);
                     sq[it] = *reinterpret_cast<const uint4*>(q + tq);
-                    sv[it] = *reinterpret_cast<const uint4*>(v + (size_t)(tb + r) * v_stride + (size_t)h * D + m * 8);
                 }
             }
             // K buffer x & 1 was last read by the update of chunk x - 2
@@ -582,6 +590,13 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
 #pragma unroll
             for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.qb[4 * it + gq][m * 8]) = sq[it];
             signal(&sm.cnt[CNT_STG_KQ], lane);
+            uint4 sv[SITEMS];
+#pragma unroll
+            for (int it = 0; it < SITEMS; ++it) {
+                const int r = 4 * it + gq;
+                sv[it] = uint4{0, 0, 0, 0};
+                if (r < L) sv[it] = *reinterpret_cast<const uint4*>(v + (size_t)(tb + r) * v_stride + (size_t)h * D + m * 8);
+            }
             wait_ge(&sm.cnt[CNT_VFREE], (unsigned)(NS * x));
 #pragma unroll
             for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.vb[4 * it + gq][m * 8]) = sv[it];
