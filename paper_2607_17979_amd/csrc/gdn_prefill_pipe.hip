@@ -164,19 +164,12 @@ __device__ __forceinline__ bf16x8_t blk_frag_t(const uint16_t (*blocks)[16][16],
 // element i = X[4 g + i][m]) is the B operand of X and the A operand of X^T
 // (contraction index 4 g + i), so prod(acc(X), acc(Y)) = acc(X^T Y).
 
-// 16 x 16 x 16 product of fp32 operands on bf16 MFMA with each operand split
-// into hi + lo (hi*hi + hi*lo + lo*hi; relative error ~2^-16).
-__device__ __forceinline__ f32x4_t prod3(const f32x4_t& a, const f32x4_t& b, f32x4_t acc) {
-    uint2 ah, al, bh, bl;
-    split_pair(a[0], a[1], ah.x, al.x);
-    split_pair(a[2], a[3], ah.y, al.y);
-    split_pair(b[0], b[1], bh.x, bl.x);
-    split_pair(b[2], b[3], bh.y, bl.y);
-    const s16x4_t ahf = __builtin_bit_cast(s16x4_t, ah), alf = __builtin_bit_cast(s16x4_t, al);
-    const s16x4_t bhf = __builtin_bit_cast(s16x4_t, bh), blf = __builtin_bit_cast(s16x4_t, bl);
-    acc = mma(ahf, bhf, acc);
-    acc = mma(ahf, blf, acc);
-    return mma(alf, bhf, acc);
+// 16 x 16 x 16 product in fp32: four 16x16x4 fp32 MFMAs, step s contracting
+// indices 4 g + s.
+__device__ __forceinline__ f32x4_t prodf(const f32x4_t& a, const f32x4_t& b, f32x4_t acc) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) acc = mma_f32(a[s], b[s], acc);
+    return acc;
 }
 
 __device__ __forceinline__ bf16x8_t as_frag(const uint4& u) { return __builtin_bit_cast(bf16x8_t, u); }
@@ -276,12 +269,18 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     ks[ct][vt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
                     ot[vt][ct] = f32x4_t{0.f, 0.f, 0.f, 0.f};
                 }
-            bf16x8_t ak[2][NCT], aq[2][NCT];  // operands of two contraction steps in flight
+            // Software pipeline over the contraction: the operands and the
+            // hi/lo split of step kq + 1 are prepared while the products of
+            // step kq run, interleaved by the scheduling groups below.
+            bf16x8_t ak[2][NCT], aq[2][NCT], bh[2][NVT], bl[2][NVT];
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) {
                 ak[0][ct] = lds_frag_perm<32>(&kb[16 * ct + m][0], 0, gq);
                 aq[0][ct] = lds_frag_perm<32>(&sm.qb[16 * ct + m][0], 0, gq);
             }
+#pragma unroll
+            for (int vt = 0; vt < NVT; ++vt) acc_frag<32>(st[0][vt], st[1][vt], bh[0][vt], bl[0][vt]);
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int kq = 0; kq < D / 32; ++kq) {
                 const int cur = kq & 1;
@@ -291,18 +290,24 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                         ak[cur ^ 1][ct] = lds_frag_perm<32>(&kb[16 * ct + m][0], 32 * (kq + 1), gq);
                         aq[cur ^ 1][ct] = lds_frag_perm<32>(&sm.qb[16 * ct + m][0], 32 * (kq + 1), gq);
                     }
-                }
-                bf16x8_t bh[NVT], bl[NVT];
 #pragma unroll
-                for (int vt = 0; vt < NVT; ++vt) acc_frag<32>(st[2 * kq][vt], st[2 * kq + 1][vt], bh[vt], bl[vt]);
+                    for (int vt = 0; vt < NVT; ++vt)
+                        acc_frag<32>(st[2 * kq + 2][vt], st[2 * kq + 3][vt], bh[cur ^ 1][vt], bl[cur ^ 1][vt]);
+                }
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
                     for (int vt = 0; vt < NVT; ++vt) {
-                        ks[ct][vt] = mma(ak[cur][ct], bh[vt], ks[ct][vt]);
-                        ks[ct][vt] = mma(ak[cur][ct], bl[vt], ks[ct][vt]);
-                        ot[vt][ct] = mma(bh[vt], aq[cur][ct], ot[vt][ct]);
+                        ks[ct][vt] = mma(ak[cur][ct], bh[cur][vt], ks[ct][vt]);
+                        ks[ct][vt] = mma(ak[cur][ct], bl[cur][vt], ks[ct][vt]);
+                        ot[vt][ct] = mma(bh[cur][vt], aq[cur][ct], ot[vt][ct]);
                     }
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);   // MFMA
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
+                    __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   // VALU
+                }
             }
             signal(&sm.cnt[CNT_QFREE], lane);
             // W = V - diag(exp(gamma)) K S0^T (in ks)
@@ -427,23 +432,25 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
         for (int x = pw, j = 0; x < nch; x += NP, ++j) {
             const int L = min(C, seq_len - x * C);
             const int tb = seq_beg + x * C;
-            // ---- inputs: gates and the K, Q operand fragments of the chunk
-            //      (fk[b][kq]: row 16 b + m, columns 32 kq + 8 gq .. + 7)
+            // ---- inputs: gates and the K operand fragments of the chunk
+            //      (fk[b][kq]: row 16 b + m, columns 32 kq + 8 gq .. + 7); the Q
+            //      fragments of block row b are loaded one block row ahead
             const bool in = lane < L;
             const float gl = in ? g[(size_t)(tb + lane) * H_v + h] : 0.f;
             const float bl = in ? beta[(size_t)(tb + lane) * H_v + h] : 0.f;
-            uint4 fk[NCT][4], fq[NCT][4];
-#pragma unroll
-            for (int b = 0; b < NCT; ++b)
+            auto load_frags = [&](const uint16_t* src, int b, uint4 (&f)[4]) {
 #pragma unroll
                 for (int kq = 0; kq < 4; ++kq) {
-                    fk[b][kq] = fq[b][kq] = uint4{0, 0, 0, 0};
-                    if (16 * b + m < L) {
-                        const size_t off = (size_t)(tb + 16 * b + m) * qk_stride + (size_t)hq * D + 32 * kq + 8 * gq;
-                        fk[b][kq] = *reinterpret_cast<const uint4*>(k + off);
-                        fq[b][kq] = *reinterpret_cast<const uint4*>(q + off);
-                    }
+                    f[kq] = uint4{0, 0, 0, 0};
+                    if (16 * b + m < L)
+                        f[kq] = *reinterpret_cast<const uint4*>(
+                            src + (size_t)(tb + 16 * b + m) * qk_stride + (size_t)hq * D + 32 * kq + 8 * gq);
                 }
+            };
+            uint4 fk[NCT][4], fq[2][4];
+#pragma unroll
+            for (int b = 0; b < NCT; ++b) load_frags(k, b, fk[b]);
+            load_frags(q, 0, fq[0]);
             const float gx = wave_prefix_sum(gl);
             const float glast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gx), C - 1));
             gam[lane] = gx;
@@ -458,12 +465,13 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             //      s = 16 jt + 4 gq + i, packed to bf16 as row t of the block
             uint2 pk[NBLK];
 #pragma unroll
-            for (int b = 0; b < NCT; ++b)
+            for (int b = 0; b < NCT; ++b) {
+                if (b + 1 < NCT) load_frags(q, b + 1, fq[(b + 1) & 1]);
 #pragma unroll
                 for (int jt = 0; jt <= b; ++jt) {
                     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                    for (int kq = 0; kq < 4; ++kq) acc = mma(as_frag(fk[jt][kq]), as_frag(fq[b][kq]), acc);
+                    for (int kq = 0; kq < 4; ++kq) acc = mma(as_frag(fk[jt][kq]), as_frag(fq[b & 1][kq]), acc);
                     const f32x4_t gc = *reinterpret_cast<const f32x4_t*>(&gam[16 * jt + 4 * gq]);
                     float val[4];
 #pragma unroll
@@ -471,23 +479,20 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                         val[i] = (jt < b || 4 * gq + i <= m) ? fast_exp(gr[b] - gc[i]) * acc[i] : 0.f;
                     pk[bidx(b, jt)] = uint2{cvt_pk(val[0], val[1]), cvt_pk(val[2], val[3])};
                 }
+            }
             // ---- A = beta_r exp(gamma_r - gamma_c) (K K^T)_rc, c < r.
-            //      Diagonal blocks N_b: acc(N_b) and acc(N_b^T) from the same
-            //      (symmetric) Gram tile.  Below the diagonal: acc(A_bk^T).
-            f32x4_t nn[NCT], nt[NCT], at[NBLK];
+            //      Diagonal blocks: acc(N_b^T) from the (symmetric) Gram tile;
+            //      below the diagonal: acc(A_bk^T).
+            f32x4_t nt[NCT], at[NBLK];
 #pragma unroll
             for (int b = 0; b < NCT; ++b) {
                 f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int kq = 0; kq < 4; ++kq) acc = mma(as_frag(fk[b][kq]), as_frag(fk[b][kq]), acc);
                 const f32x4_t gc = *reinterpret_cast<const f32x4_t*>(&gam[16 * b + 4 * gq]);
-                const f32x4_t bc = *reinterpret_cast<const f32x4_t*>(&bet[16 * b + 4 * gq]);
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int r = 4 * gq + i;
-                    nn[b][i] = (m < r) ? bc[i] * fast_exp(gc[i] - gr[b]) * acc[i] : 0.f;
-                    nt[b][i] = (r < m) ? br[b] * fast_exp(gr[b] - gc[i]) * acc[i] : 0.f;
-                }
+                for (int i = 0; i < 4; ++i)
+                    nt[b][i] = (4 * gq + i < m) ? br[b] * fast_exp(gr[b] - gc[i]) * acc[i] : 0.f;
 #pragma unroll
                 for (int kb = 0; kb < b; ++kb) {
                     f32x4_t ag = {0.f, 0.f, 0.f, 0.f};
@@ -501,7 +506,8 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             // ---- T = (I + A)^-1: diagonal blocks D_b = (I + N_b)^-1 by forward
             //      substitution in fp32, lane 16 b + j solving column j of
             //      block b (rows of N_b are read as LDS broadcasts); then block
-            //      columns T_bJ = -D_b sum_{kb=J}^{b-1} A_{b,kb} T_{kb,J} (b > J).
+            //      columns T_bJ = -D_b sum_{kb=J}^{b-1} A_{b,kb} T_{kb,J} (b > J)
+            //      on fp32 MFMA.
             float* scb = scr + gq * 16 * SP;  // this lane's block b = gq
 #pragma unroll
             for (int b = 0; b < NCT; ++b)     // row m of N_b, columns 4 gq .. 4 gq + 3
@@ -538,18 +544,15 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     for (int i = 0; i < 4; ++i) ddt[b][i] = -scr[(16 * b + 4 * gq + i) * SP + m];
                 }
             }
-            {
-                const f32x4_t zero4 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int bi = 1; bi < NCT; ++bi)
+            for (int bi = 1; bi < NCT; ++bi)
 #pragma unroll
-                    for (int J = 0; J < bi; ++J) {
-                        f32x4_t y = prod3(at[bidx(bi, J)], dd[J], zero4);
+                for (int J = 0; J < bi; ++J) {
+                    f32x4_t y = prodf(at[bidx(bi, J)], dd[J], f32x4_t{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
-                        for (int kb = J + 1; kb < bi; ++kb) y += prod3(at[bidx(bi, kb)], tt[bidx(kb, J)], zero4);
-                        tt[bidx(bi, J)] = prod3(ddt[bi], y, zero4);
-                    }
-            }
+                    for (int kb = J + 1; kb < bi; ++kb) y = prodf(at[bidx(bi, kb)], tt[bidx(kb, J)], y);
+                    tt[bidx(bi, J)] = prodf(ddt[bi], y, f32x4_t{0.f, 0.f, 0.f, 0.f});
+                }
             // ---- publish to the slot once the state waves are done with its
             //      previous chunk
             wait_ge(&sm.cnt[CNT_SFREE0 + pw], (unsigned)(NS * j));
