@@ -185,6 +185,204 @@ __device__ __forceinline__ void store_split_t(uint16_t (*th)[16], uint16_t (*tl)
     *reinterpret_cast<uint2*>(&tl[m][4 * g]) = lo;
 }
 
+// Context of a producer wave: values fixed for the whole sequence.
+struct ProdCtx {
+    const uint16_t* q;
+    const uint16_t* k;
+    const uint16_t* v;
+    const float* g;
+    const float* beta;
+    size_t qk_stride, v_stride;
+    int seq_beg, seq_len, hq, h, H_v, pw;
+};
+
+// Producer work for chunk x (the j-th chunk of producer pc.pw).  The lane
+// indices m, gq are passed in per chunk (opaque to the compiler), so the
+// addresses and masks derived from them are recomputed per chunk instead of
+// being kept live across the producer loop.
+template <int NS>
+__device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x, int j, int m, int gq) {
+    const int lane = m + 16 * gq;
+    Slot& sl = sm.slot[pc.pw];
+    float* scr = sm.scr[pc.pw];
+    float* gam = sm.gam[pc.pw];
+    float* bet = sm.bet[pc.pw];
+    const int L = min(C, pc.seq_len - x * C);
+    const int tb = pc.seq_beg + x * C;
+    // ---- inputs: gates and the K operand fragments of the chunk
+    //      (fk[b][kq]: row 16 b + m, columns 32 kq + 8 gq .. + 7); the Q
+    //      fragments of block row b are loaded one block row ahead
+    const bool in = lane < L;
+    const float gl = in ? pc.g[(size_t)(tb + lane) * pc.H_v + pc.h] : 0.f;
+    const float bl = in ? pc.beta[(size_t)(tb + lane) * pc.H_v + pc.h] : 0.f;
+    auto load_frags = [&](const uint16_t* src, int b, uint4 (&f)[4]) {
+#pragma unroll
+        for (int kq = 0; kq < 4; ++kq) {
+            f[kq] = uint4{0, 0, 0, 0};
+            if (16 * b + m < L)
+                f[kq] = *reinterpret_cast<const uint4*>(
+                    src + (size_t)(tb + 16 * b + m) * pc.qk_stride + (size_t)pc.hq * D + 32 * kq + 8 * gq);
+        }
+    };
+    uint4 fk[NCT][4], fq[2][4];
+#pragma unroll
+    for (int b = 0; b < NCT; ++b) load_frags(pc.k, b, fk[b]);
+    load_frags(pc.q, 0, fq[0]);
+    const float gx = wave_prefix_sum(gl);
+    const float glast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gx), C - 1));
+    gam[lane] = gx;
+    bet[lane] = bl;
+    float gr[NCT], br[NCT];  // gamma, beta of row 16 b + m
+#pragma unroll
+    for (int b = 0; b < NCT; ++b) {
+        gr[b] = gam[16 * b + m];
+        br[b] = bet[16 * b + m];
+    }
+    // ---- masked scores: tile (b, jt) of (M o Q K^T)^T, t = 16 b + m,
+    //      s = 16 jt + 4 gq + i, packed to bf16 as row t of the block
+    uint2 pk[NBLK];
+#pragma unroll
+    for (int b = 0; b < NCT; ++b) {
+        if (b + 1 < NCT) load_frags(pc.q, b + 1, fq[(b + 1) & 1]);
+#pragma unroll
+        for (int jt = 0; jt <= b; ++jt) {
+            f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kq = 0; kq < 4; ++kq) acc = mma(as_frag(fk[jt][kq]), as_frag(fq[b & 1][kq]), acc);
+            const f32x4_t gc = *reinterpret_cast<const f32x4_t*>(&gam[16 * jt + 4 * gq]);
+            float val[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                val[i] = (jt < b || 4 * gq + i <= m) ? fast_exp(gr[b] - gc[i]) * acc[i] : 0.f;
+            pk[bidx(b, jt)] = uint2{cvt_pk(val[0], val[1]), cvt_pk(val[2], val[3])};
+        }
+    }
+    // ---- A = beta_r exp(gamma_r - gamma_c) (K K^T)_rc, c < r.
+    //      Diagonal blocks: acc(N_b^T) from the (symmetric) Gram tile;
+    //      below the diagonal: acc(A_bk^T).
+    f32x4_t nt[NCT], at[NBLK];
+#pragma unroll
+    for (int b = 0; b < NCT; ++b) {
+        f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kq = 0; kq < 4; ++kq) acc = mma(as_frag(fk[b][kq]), as_frag(fk[b][kq]), acc);
+        const f32x4_t gc = *reinterpret_cast<const f32x4_t*>(&gam[16 * b + 4 * gq]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            nt[b][i] = (4 * gq + i < m) ? br[b] * fast_exp(gr[b] - gc[i]) * acc[i] : 0.f;
+#pragma unroll
+        for (int kb = 0; kb < b; ++kb) {
+            f32x4_t ag = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kq = 0; kq < 4; ++kq) ag = mma(as_frag(fk[kb][kq]), as_frag(fk[b][kq]), ag);
+            const f32x4_t gk = *reinterpret_cast<const f32x4_t*>(&gam[16 * kb + 4 * gq]);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) at[bidx(b, kb)][i] = br[b] * fast_exp(gr[b] - gk[i]) * ag[i];
+        }
+    }
+    // ---- T = (I + A)^-1: diagonal blocks D_b = (I + N_b)^-1 by forward
+    //      substitution in fp32, lane 16 b + j solving column j of
+    //      block b (rows of N_b are read as LDS broadcasts); then block
+    //      columns T_bJ = -D_b sum_{kb=J}^{b-1} A_{b,kb} T_{kb,J} (b > J)
+    //      on fp32 MFMA.
+    float* scb = scr + gq * 16 * SP;  // this lane's block b = gq
+#pragma unroll
+    for (int b = 0; b < NCT; ++b)     // row m of N_b, columns 4 gq .. 4 gq + 3
+        *reinterpret_cast<f32x4_t*>(&scr[(16 * b + m) * SP + 4 * gq]) = nt[b];
+    // Row r + 1 of N_b is read while row r is solved; the scheduling
+    // fences keep the reads from being hoisted all at once.
+    float xs[16];
+    f32x4_t nrow[2][4];
+    xs[0] = (m == 0) ? 1.f : 0.f;
+    nrow[1][0] = *reinterpret_cast<const f32x4_t*>(&scb[1 * SP]);
+#pragma unroll
+    for (int r = 1; r < 16; ++r) {
+        const int cur = r & 1;
+        if (r + 1 < 16) {
+#pragma unroll
+            for (int i4 = 0; i4 < r + 1; i4 += 4)
+                nrow[cur ^ 1][i4 / 4] = *reinterpret_cast<const f32x4_t*>(&scb[(r + 1) * SP + i4]);
+        }
+        float acc = (r == m) ? 1.f : 0.f;
+#pragma unroll
+        for (int i = 0; i < r; ++i) acc = fmaf(-nrow[cur][i / 4][i % 4], xs[i], acc);
+        xs[r] = acc;
+        __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int r4 = 0; r4 < 16; r4 += 4)  // row m of the scratch block = column m of D_b
+        *reinterpret_cast<f32x4_t*>(&scb[m * SP + r4]) = f32x4_t{xs[r4], xs[r4 + 1], xs[r4 + 2], xs[r4 + 3]};
+    f32x4_t dd[NCT], ddt[NCT], tt[NBLK];
+#pragma unroll
+    for (int b = 0; b < NCT; ++b) {     // acc(D_b): D_b[4 gq + i][m]
+        dd[b] = *reinterpret_cast<const f32x4_t*>(&scr[(16 * b + m) * SP + 4 * gq]);
+        if (b > 0) {                    // -acc(D_b^T): -D_b[m][4 gq + i]
+#pragma unroll
+            for (int i = 0; i < 4; ++i) ddt[b][i] = -scr[(16 * b + 4 * gq + i) * SP + m];
+        }
+    }
+#pragma unroll
+    for (int bi = 1; bi < NCT; ++bi)
+#pragma unroll
+        for (int J = 0; J < bi; ++J) {
+            f32x4_t y = prodf(at[bidx(bi, J)], dd[J], f32x4_t{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+            for (int kb = J + 1; kb < bi; ++kb) y = prodf(at[bidx(bi, kb)], tt[bidx(kb, J)], y);
+            tt[bidx(bi, J)] = prodf(ddt[bi], y, f32x4_t{0.f, 0.f, 0.f, 0.f});
+        }
+    // ---- publish to the slot once the state waves are done with its
+    //      previous chunk
+    wait_ge(&sm.cnt[CNT_SFREE0 + pc.pw], (unsigned)(NS * j));
+#pragma unroll
+    for (int b = 0; b < NCT; ++b)
+#pragma unroll
+        for (int jt = 0; jt <= b; ++jt)
+            *reinterpret_cast<uint2*>(&sl.pm[bidx(b, jt)][m][4 * gq]) = pk[bidx(b, jt)];
+#pragma unroll
+    for (int b = 0; b < NCT; ++b) {
+        store_split_t(sl.th[bidx(b, b)], sl.tl[bidx(b, b)], dd[b], br[b], m, gq);
+#pragma unroll
+        for (int J = 0; J < b; ++J) store_split_t(sl.th[bidx(b, J)], sl.tl[bidx(b, J)], tt[bidx(b, J)], br[J], m, gq);
+    }
+    sl.eg[lane] = fast_exp(gx);
+    sl.egl[lane] = fast_exp(glast - gx);
+    signal(&sm.cnt[CNT_READY0 + pc.pw], lane);
+    // ---- stage the chunk's K, Q, V rows once the state waves have
+    //      released the previous chunk's (row 4 it + gq, segment m);
+    //      chunk 0 was staged by the whole workgroup
+    if (x == 0) return;
+    uint4 sk[SITEMS], sq[SITEMS];
+#pragma unroll
+    for (int it = 0; it < SITEMS; ++it) {
+        const int r = 4 * it + gq;
+        sk[it] = sq[it] = uint4{0, 0, 0, 0};
+        if (r < L) {
+            const size_t tq = (size_t)(tb + r) * pc.qk_stride + (size_t)pc.hq * D + m * 8;
+            sk[it] = *reinterpret_cast<const uint4*>(pc.k + tq);
+            sq[it] = *reinterpret_cast<const uint4*>(pc.q + tq);
+        }
+    }
+    // K buffer x & 1 was last read by the update of chunk x - 2
+    wait_ge(&sm.cnt[CNT_KFREE], (unsigned)(x >= 2 ? NS * (x - 1) : 0));
+#pragma unroll
+    for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.kb[x & 1][4 * it + gq][m * 8]) = sk[it];
+    wait_ge(&sm.cnt[CNT_QFREE], (unsigned)(NS * x));
+#pragma unroll
+    for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.qb[4 * it + gq][m * 8]) = sq[it];
+    signal(&sm.cnt[CNT_STG_KQ], lane);
+    uint4 sv[SITEMS];
+#pragma unroll
+    for (int it = 0; it < SITEMS; ++it) {
+        const int r = 4 * it + gq;
+        sv[it] = uint4{0, 0, 0, 0};
+        if (r < L) sv[it] = *reinterpret_cast<const uint4*>(pc.v + (size_t)(tb + r) * pc.v_stride + (size_t)pc.h * D + m * 8);
+    }
+    wait_ge(&sm.cnt[CNT_VFREE], (unsigned)(NS * x));
+#pragma unroll
+    for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.vb[4 * it + gq][m * 8]) = sv[it];
+    signal(&sm.cnt[CNT_STG_V], lane);
+}
+
 // NS state waves (4 or 8), each owning D / NS value columns.
 template <int NS>
 __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
@@ -328,17 +526,20 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     for (int i = 0; i < 4; ++i) ks[ct][vt][i] = fmaf(-egr[ct][i], ks[ct][vt][i], vf[i]);
                 }
             signal(&sm.cnt[CNT_VFREE], lane);
-            // U = T diag(beta) W  (hi*hi + hi*lo + lo*hi)
+            // U = T diag(beta) W  (hi*hi + hi*lo + lo*hi); the split of the
+            // second half of W overlaps the products of the first.
             f32x4_t uu[NCT][NVT];
+            bf16x8_t wh[2][NVT], wl[2][NVT];
 #pragma unroll
-            for (int ct = 0; ct < NCT; ++ct)
-#pragma unroll
-                for (int vt = 0; vt < NVT; ++vt) uu[ct][vt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            for (int vt = 0; vt < NVT; ++vt) acc_frag<32>(ks[0][vt], ks[1][vt], wh[0][vt], wl[0][vt]);
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int kc = 0; kc < C; kc += 32) {
-                bf16x8_t wh[NVT], wl[NVT];
+                const int hb = kc / 32;
+                if (hb == 0) {
 #pragma unroll
-                for (int vt = 0; vt < NVT; ++vt) acc_frag<32>(ks[kc / 16][vt], ks[kc / 16 + 1][vt], wh[vt], wl[vt]);
+                    for (int vt = 0; vt < NVT; ++vt) acc_frag<32>(ks[2][vt], ks[3][vt], wh[1][vt], wl[1][vt]);
+                }
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) {
                     if (kc > 16 * ct + 15) continue;
@@ -346,13 +547,51 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     const bf16x8_t al = blk_frag_t(sl.tl, sm.zero, ct, kc, m, gq);
 #pragma unroll
                     for (int vt = 0; vt < NVT; ++vt) {
-                        uu[ct][vt] = mma(ah, wh[vt], uu[ct][vt]);
-                        uu[ct][vt] = mma(ah, wl[vt], uu[ct][vt]);
-                        uu[ct][vt] = mma(al, wh[vt], uu[ct][vt]);
+                        const f32x4_t u0 = (kc == 0) ? f32x4_t{0.f, 0.f, 0.f, 0.f} : uu[ct][vt];
+                        uu[ct][vt] = mma(ah, wh[hb][vt], u0);
+                        uu[ct][vt] = mma(ah, wl[hb][vt], uu[ct][vt]);
+                        uu[ct][vt] = mma(al, wh[hb][vt], uu[ct][vt]);
+                    }
+                }
+                if (hb == 0) {
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) {
+                        __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);   // MFMA
+                        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
+                        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   // VALU
                     }
                 }
             }
-            // O^T = diag(exp(gamma)) (Q S0^T)^T + U^T (M o Q K^T)^T  (U hi)
+            // S^T = exp(gamma_last) S^T + K^T (diag(exp(gamma_last - gamma)) U)   (hi + lo),
+            // block row by block row of S^T so that the scaling of one overlaps
+            // the products of the previous
+            f32x4_t eglv[NCT];
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) eglv[ct] = *reinterpret_cast<const f32x4_t*>(&sl.egl[16 * ct + 4 * gq]);
+            const float eg_last = sl.eg[C - 1];
+            bf16x8_t uth[2][NVT], utl[2][NVT];
+#pragma unroll
+            for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+                for (int vt = 0; vt < NVT; ++vt)
+                    acc_frag<32>(uu[2 * hb][vt] * eglv[2 * hb], uu[2 * hb + 1][vt] * eglv[2 * hb + 1], uth[hb][vt], utl[hb][vt]);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) {
+                const bf16x8_t a0 = lds_frag_tr(kb, 0, 16 * dt, m, gq);
+                const bf16x8_t a1 = lds_frag_tr(kb, 32, 16 * dt, m, gq);
+#pragma unroll
+                for (int vt = 0; vt < NVT; ++vt) {
+                    st[dt][vt] *= eg_last;
+                    st[dt][vt] = mma(a0, uth[0][vt], st[dt][vt]);
+                    st[dt][vt] = mma(a0, utl[0][vt], st[dt][vt]);
+                    st[dt][vt] = mma(a1, uth[1][vt], st[dt][vt]);
+                    st[dt][vt] = mma(a1, utl[1][vt], st[dt][vt]);
+                }
+            }
+            signal(&sm.cnt[CNT_KFREE], lane);
+            // O^T = diag(exp(gamma)) (Q S0^T)^T + U^T (M o Q K^T)^T  (U hi); its
+            // vector work overlaps the update's products
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) {
                 const float e = sl.eg[16 * ct + m];
@@ -372,6 +611,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     for (int vt = 0; vt < NVT; ++vt) ot[vt][ct] = mma(uh[vt], bp, ot[vt][ct]);
                 }
             }
+            signal(&sm.cnt[CNT_SFREE0 + c % NP], lane);
             // Outputs: lane m + 16 gq holds token 16 ct + m, value columns 4 gq .. 4 gq + 3.
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) {
@@ -386,33 +626,6 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     }
                 }
             }
-            // S^T = exp(gamma_last) S^T + K^T (diag(exp(gamma_last - gamma)) U)   (hi + lo)
-            f32x4_t eglv[NCT];
-#pragma unroll
-            for (int ct = 0; ct < NCT; ++ct) eglv[ct] = *reinterpret_cast<const f32x4_t*>(&sl.egl[16 * ct + 4 * gq]);
-            const float eg_last = sl.eg[C - 1];
-            signal(&sm.cnt[CNT_SFREE0 + c % NP], lane);
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-                for (int vt = 0; vt < NVT; ++vt) st[dt][vt] *= eg_last;
-#pragma unroll
-            for (int kc = 0; kc < C; kc += 32) {
-                bf16x8_t uth[NVT], utl[NVT];
-#pragma unroll
-                for (int vt = 0; vt < NVT; ++vt)
-                    acc_frag<32>(uu[kc / 16][vt] * eglv[kc / 16], uu[kc / 16 + 1][vt] * eglv[kc / 16 + 1], uth[vt], utl[vt]);
-#pragma unroll
-                for (int dt = 0; dt < NDT; ++dt) {
-                    const bf16x8_t a = lds_frag_tr(kb, kc, 16 * dt, m, gq);
-#pragma unroll
-                    for (int vt = 0; vt < NVT; ++vt) {
-                        st[dt][vt] = mma(a, uth[vt], st[dt][vt]);
-                        st[dt][vt] = mma(a, utl[vt], st[dt][vt]);
-                    }
-                }
-            }
-            signal(&sm.cnt[CNT_KFREE], lane);
         }
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt)
@@ -424,186 +637,11 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             }
     } else {
         // ======================= producer waves ================================
-        const int pw = wave - NS;
-        Slot& sl = sm.slot[pw];
-        float* scr = sm.scr[pw];
-        float* gam = sm.gam[pw];
-        float* bet = sm.bet[pw];
-        for (int x = pw, j = 0; x < nch; x += NP, ++j) {
-            const int L = min(C, seq_len - x * C);
-            const int tb = seq_beg + x * C;
-            // ---- inputs: gates and the K operand fragments of the chunk
-            //      (fk[b][kq]: row 16 b + m, columns 32 kq + 8 gq .. + 7); the Q
-            //      fragments of block row b are loaded one block row ahead
-            const bool in = lane < L;
-            const float gl = in ? g[(size_t)(tb + lane) * H_v + h] : 0.f;
-            const float bl = in ? beta[(size_t)(tb + lane) * H_v + h] : 0.f;
-            auto load_frags = [&](const uint16_t* src, int b, uint4 (&f)[4]) {
-#pragma unroll
-                for (int kq = 0; kq < 4; ++kq) {
-                    f[kq] = uint4{0, 0, 0, 0};
-                    if (16 * b + m < L)
-                        f[kq] = *reinterpret_cast<const uint4*>(
-                            src + (size_t)(tb + 16 * b + m) * qk_stride + (size_t)hq * D + 32 * kq + 8 * gq);
-                }
-            };
-            uint4 fk[NCT][4], fq[2][4];
-#pragma unroll
-            for (int b = 0; b < NCT; ++b) load_frags(k, b, fk[b]);
-            load_frags(q, 0, fq[0]);
-            const float gx = wave_prefix_sum(gl);
-            const float glast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gx), C - 1));
-            gam[lane] = gx;
-            bet[lane] = bl;
-            float gr[NCT], br[NCT];  // gamma, beta of row 16 b + m
-#pragma unroll
-            for (int b = 0; b < NCT; ++b) {
-                gr[b] = gam[16 * b + m];
-                br[b] = bet[16 * b + m];
-            }
-            // ---- masked scores: tile (b, jt) of (M o Q K^T)^T, t = 16 b + m,
-            //      s = 16 jt + 4 gq + i, packed to bf16 as row t of the block
-            uint2 pk[NBLK];
-#pragma unroll
-            for (int b = 0; b < NCT; ++b) {
-                if (b + 1 < NCT) load_frags(q, b + 1, fq[(b + 1) & 1]);
-#pragma unroll
-                for (int jt = 0; jt <= b; ++jt) {
-                    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int kq = 0; kq < 4; ++kq) acc = mma(as_frag(fk[jt][kq]), as_frag(fq[b & 1][kq]), acc);
-                    const f32x4_t gc = *reinterpret_cast<const f32x4_t*>(&gam[16 * jt + 4 * gq]);
-                    float val[4];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        val[i] = (jt < b || 4 * gq + i <= m) ? fast_exp(gr[b] - gc[i]) * acc[i] : 0.f;
-                    pk[bidx(b, jt)] = uint2{cvt_pk(val[0], val[1]), cvt_pk(val[2], val[3])};
-                }
-            }
-            // ---- A = beta_r exp(gamma_r - gamma_c) (K K^T)_rc, c < r.
-            //      Diagonal blocks: acc(N_b^T) from the (symmetric) Gram tile;
-            //      below the diagonal: acc(A_bk^T).
-            f32x4_t nt[NCT], at[NBLK];
-#pragma unroll
-            for (int b = 0; b < NCT; ++b) {
-                f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int kq = 0; kq < 4; ++kq) acc = mma(as_frag(fk[b][kq]), as_frag(fk[b][kq]), acc);
-                const f32x4_t gc = *reinterpret_cast<const f32x4_t*>(&gam[16 * b + 4 * gq]);
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    nt[b][i] = (4 * gq + i < m) ? br[b] * fast_exp(gr[b] - gc[i]) * acc[i] : 0.f;
-#pragma unroll
-                for (int kb = 0; kb < b; ++kb) {
-                    f32x4_t ag = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int kq = 0; kq < 4; ++kq) ag = mma(as_frag(fk[kb][kq]), as_frag(fk[b][kq]), ag);
-                    const f32x4_t gk = *reinterpret_cast<const f32x4_t*>(&gam[16 * kb + 4 * gq]);
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) at[bidx(b, kb)][i] = br[b] * fast_exp(gr[b] - gk[i]) * ag[i];
-                }
-            }
-            // ---- T = (I + A)^-1: diagonal blocks D_b = (I + N_b)^-1 by forward
-            //      substitution in fp32, lane 16 b + j solving column j of
-            //      block b (rows of N_b are read as LDS broadcasts); then block
-            //      columns T_bJ = -D_b sum_{kb=J}^{b-1} A_{b,kb} T_{kb,J} (b > J)
-            //      on fp32 MFMA.
-            float* scb = scr + gq * 16 * SP;  // this lane's block b = gq
-#pragma unroll
-            for (int b = 0; b < NCT; ++b)     // row m of N_b, columns 4 gq .. 4 gq + 3
-                *reinterpret_cast<f32x4_t*>(&scr[(16 * b + m) * SP + 4 * gq]) = nt[b];
-            // Row r + 1 of N_b is read while row r is solved; the scheduling
-            // fences keep the reads from being hoisted all at once.
-            float xs[16];
-            f32x4_t nrow[2][4];
-            xs[0] = (m == 0) ? 1.f : 0.f;
-            nrow[1][0] = *reinterpret_cast<const f32x4_t*>(&scb[1 * SP]);
-#pragma unroll
-            for (int r = 1; r < 16; ++r) {
-                const int cur = r & 1;
-                if (r + 1 < 16) {
-#pragma unroll
-                    for (int i4 = 0; i4 < r + 1; i4 += 4)
-                        nrow[cur ^ 1][i4 / 4] = *reinterpret_cast<const f32x4_t*>(&scb[(r + 1) * SP + i4]);
-                }
-                float acc = (r == m) ? 1.f : 0.f;
-#pragma unroll
-                for (int i = 0; i < r; ++i) acc = fmaf(-nrow[cur][i / 4][i % 4], xs[i], acc);
-                xs[r] = acc;
-                __builtin_amdgcn_sched_barrier(0);
-            }
-#pragma unroll
-            for (int r4 = 0; r4 < 16; r4 += 4)  // row m of the scratch block = column m of D_b
-                *reinterpret_cast<f32x4_t*>(&scb[m * SP + r4]) = f32x4_t{xs[r4], xs[r4 + 1], xs[r4 + 2], xs[r4 + 3]};
-            f32x4_t dd[NCT], ddt[NCT], tt[NBLK];
-#pragma unroll
-            for (int b = 0; b < NCT; ++b) {     // acc(D_b): D_b[4 gq + i][m]
-                dd[b] = *reinterpret_cast<const f32x4_t*>(&scr[(16 * b + m) * SP + 4 * gq]);
-                if (b > 0) {                    // -acc(D_b^T): -D_b[m][4 gq + i]
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) ddt[b][i] = -scr[(16 * b + 4 * gq + i) * SP + m];
-                }
-            }
-#pragma unroll
-            for (int bi = 1; bi < NCT; ++bi)
-#pragma unroll
-                for (int J = 0; J < bi; ++J) {
-                    f32x4_t y = prodf(at[bidx(bi, J)], dd[J], f32x4_t{0.f, 0.f, 0.f, 0.f});
-#pragma unroll
-                    for (int kb = J + 1; kb < bi; ++kb) y = prodf(at[bidx(bi, kb)], tt[bidx(kb, J)], y);
-                    tt[bidx(bi, J)] = prodf(ddt[bi], y, f32x4_t{0.f, 0.f, 0.f, 0.f});
-                }
-            // ---- publish to the slot once the state waves are done with its
-            //      previous chunk
-            wait_ge(&sm.cnt[CNT_SFREE0 + pw], (unsigned)(NS * j));
-#pragma unroll
-            for (int b = 0; b < NCT; ++b)
-#pragma unroll
-                for (int jt = 0; jt <= b; ++jt)
-                    *reinterpret_cast<uint2*>(&sl.pm[bidx(b, jt)][m][4 * gq]) = pk[bidx(b, jt)];
-#pragma unroll
-            for (int b = 0; b < NCT; ++b) {
-                store_split_t(sl.th[bidx(b, b)], sl.tl[bidx(b, b)], dd[b], br[b], m, gq);
-#pragma unroll
-                for (int J = 0; J < b; ++J) store_split_t(sl.th[bidx(b, J)], sl.tl[bidx(b, J)], tt[bidx(b, J)], br[J], m, gq);
-            }
-            sl.eg[lane] = fast_exp(gx);
-            sl.egl[lane] = fast_exp(glast - gx);
-            signal(&sm.cnt[CNT_READY0 + pw], lane);
-            // ---- stage the chunk's K, Q, V rows once the state waves have
-            //      released the previous chunk's (row 4 it + gq, segment m);
-            //      chunk 0 was staged by the whole workgroup
-            if (x == 0) continue;
-            uint4 sk[SITEMS], sq[SITEMS];
-#pragma unroll
-            for (int it = 0; it < SITEMS; ++it) {
-                const int r = 4 * it + gq;
-                sk[it] = sq[it] = uint4{0, 0, 0, 0};
-                if (r < L) {
-                    const size_t tq = (size_t)(tb + r) * qk_stride + (size_t)hq * D + m * 8;
-                    sk[it] = *reinterpret_cast<const uint4*>(k + tq);
-                    sq[it] = *reinterpret_cast<const uint4*>(q + tq);
-                }
-            }
-            // K buffer x & 1 was last read by the update of chunk x - 2
-            wait_ge(&sm.cnt[CNT_KFREE], (unsigned)(x >= 2 ? NS * (x - 1) : 0));
-#pragma unroll
-            for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.kb[x & 1][4 * it + gq][m * 8]) = sk[it];
-            wait_ge(&sm.cnt[CNT_QFREE], (unsigned)(NS * x));
-#pragma unroll
-            for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.qb[4 * it + gq][m * 8]) = sq[it];
-            signal(&sm.cnt[CNT_STG_KQ], lane);
-            uint4 sv[SITEMS];
-#pragma unroll
-            for (int it = 0; it < SITEMS; ++it) {
-                const int r = 4 * it + gq;
-                sv[it] = uint4{0, 0, 0, 0};
-                if (r < L) sv[it] = *reinterpret_cast<const uint4*>(v + (size_t)(tb + r) * v_stride + (size_t)h * D + m * 8);
-            }
-            wait_ge(&sm.cnt[CNT_VFREE], (unsigned)(NS * x));
-#pragma unroll
-            for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.vb[4 * it + gq][m * 8]) = sv[it];
-            signal(&sm.cnt[CNT_STG_V], lane);
+        const ProdCtx pc = {q, k, v, g, beta, qk_stride, v_stride, seq_beg, seq_len, hq, h, H_v, wave - NS};
+        for (int x = wave - NS, j = 0; x < nch; x += NP, ++j) {
+            int mo = m, go = gq;
+            asm volatile("" : "+v"(mo), "+v"(go));
+            produce_chunk<NS>(sm, pc, x, j, mo, go);
         }
     }
 }
