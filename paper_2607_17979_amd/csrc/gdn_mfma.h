@@ -79,6 +79,27 @@ __device__ __forceinline__ void split_pair(float a, float b, uint32_t& hi, uint3
     lo = cvt_pk(a - __uint_as_float(hi << 16), b - __uint_as_float(hi & 0xFFFF0000u));
 }
 
+// hi / lo split with the residual from the dot-product unit: lo of element e
+// is bf16(x_e + hi . m_e) with m_0 = (-1, 0), m_1 = (0, -1) as packed bf16, one
+// v_dot2_f32_bf16 each (exact: x - hi is representable).  The two masks are
+// kept in registers (opaque to the compiler): folding them into the
+// instruction's inline-constant form placed -1 in the wrong half.
+struct SplitMasks {
+    uint32_t m0, m1;
+};
+__device__ __forceinline__ SplitMasks split_masks() {
+    uint32_t a = 0x0000BF80u, b = 0xBF800000u;
+    asm volatile("" : "+v"(a), "+v"(b));
+    return SplitMasks{a, b};
+}
+__device__ __forceinline__ void split_pair(float a, float b, uint32_t& hi, uint32_t& lo, const SplitMasks& sm) {
+    hi = cvt_pk(a, b);
+    const bf16x2_t h = __builtin_bit_cast(bf16x2_t, hi);
+    const float la = __builtin_amdgcn_fdot2_f32_bf16(h, __builtin_bit_cast(bf16x2_t, sm.m0), a, false);
+    const float lb = __builtin_amdgcn_fdot2_f32_bf16(h, __builtin_bit_cast(bf16x2_t, sm.m1), b, false);
+    lo = cvt_pk(la, lb);
+}
+
 // B operand (hi and lo parts) from accumulator tiles t0 (contraction rows
 // k0..k0+15) and t1 (rows k0+16..k0+31), in the permuted order.
 template <int K>
@@ -99,6 +120,18 @@ __device__ __forceinline__ void acc_frag(const f32x4_t& t0, const f32x4_t& t1,
         hi = __builtin_bit_cast(s16x4_t, uh);
         lo = __builtin_bit_cast(s16x4_t, ul);
     }
+}
+
+// The same with the dot-product residual.
+__device__ __forceinline__ void acc_frag(const f32x4_t& t0, const f32x4_t& t1, bf16x8_t& hi, bf16x8_t& lo,
+                                         const SplitMasks& sm) {
+    uint4 uh, ul;
+    split_pair(t0[0], t0[1], uh.x, ul.x, sm);
+    split_pair(t0[2], t0[3], uh.y, ul.y, sm);
+    split_pair(t1[0], t1[1], uh.z, ul.z, sm);
+    split_pair(t1[2], t1[3], uh.w, ul.w, sm);
+    hi = __builtin_bit_cast(bf16x8_t, uh);
+    lo = __builtin_bit_cast(bf16x8_t, ul);
 }
 
 // B operand, hi part only.

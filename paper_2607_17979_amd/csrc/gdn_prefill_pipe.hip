@@ -50,7 +50,7 @@ __device__ __forceinline__ constexpr int bidx(int i, int j) { return i * (i + 1)
 struct Slot {
     uint16_t th[NBLK][16][16];   // T diag(beta) by lower blocks, transposed [col][row], bf16 hi
     uint16_t tl[NBLK][16][16];   // bf16 lo
-    uint16_t pm[NBLK][16][16];   // (M o Q K^T) by lower blocks [row t][col s], bf16
+    uint16_t pm[NBLK][16][16];   // scale (M o Q K^T) by lower blocks [row t][col s], bf16
     alignas(16) float eg[C];     // exp(gamma)
     alignas(16) float egl[C];    // exp(gamma_last - gamma)
 };
@@ -194,6 +194,7 @@ struct ProdCtx {
     const float* beta;
     size_t qk_stride, v_stride;
     int seq_beg, seq_len, hq, h, H_v, pw;
+    float scale;
 };
 
 // Producer work for chunk x (the j-th chunk of producer pc.pw).  The lane
@@ -212,22 +213,26 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
     // ---- inputs: gates and the K operand fragments of the chunk
     //      (fk[b][kq]: row 16 b + m, columns 32 kq + 8 gq .. + 7); the Q
     //      fragments of block row b are loaded one block row ahead
+    // Uniform chunk bases with 32-bit lane offsets.  Rows past the end of a
+    // short last chunk read row L - 1 instead of zeros: those rows have
+    // g = beta = 0, so T diag(beta) is exactly zero in their rows and columns,
+    // and their scores and outputs are never used; the values only need to be
+    // finite.
+    const uint16_t* kc0 = pc.k + (size_t)tb * pc.qk_stride + (size_t)pc.hq * D;
+    const uint16_t* qc0 = pc.q + (size_t)tb * pc.qk_stride + (size_t)pc.hq * D;
+    const unsigned qks = (unsigned)pc.qk_stride;
     const bool in = lane < L;
     const float gl = in ? pc.g[(size_t)(tb + lane) * pc.H_v + pc.h] : 0.f;
     const float bl = in ? pc.beta[(size_t)(tb + lane) * pc.H_v + pc.h] : 0.f;
-    auto load_frags = [&](const uint16_t* src, int b, uint4 (&f)[4]) {
+    auto load_frags = [&](const uint16_t* base, int b, uint4 (&f)[4]) {
+        const unsigned off = (unsigned)min(16 * b + m, L - 1) * qks + 8u * gq;
 #pragma unroll
-        for (int kq = 0; kq < 4; ++kq) {
-            f[kq] = uint4{0, 0, 0, 0};
-            if (16 * b + m < L)
-                f[kq] = *reinterpret_cast<const uint4*>(
-                    src + (size_t)(tb + 16 * b + m) * pc.qk_stride + (size_t)pc.hq * D + 32 * kq + 8 * gq);
-        }
+        for (int kq = 0; kq < 4; ++kq) f[kq] = *reinterpret_cast<const uint4*>(base + off + 32 * kq);
     };
     uint4 fk[NCT][4], fq[2][4];
 #pragma unroll
-    for (int b = 0; b < NCT; ++b) load_frags(pc.k, b, fk[b]);
-    load_frags(pc.q, 0, fq[0]);
+    for (int b = 0; b < NCT; ++b) load_frags(kc0, b, fk[b]);
+    load_frags(qc0, 0, fq[0]);
     const float gx = wave_prefix_sum(gl);
     const float glast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gx), C - 1));
     gam[lane] = gx;
@@ -243,7 +248,7 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
     uint2 pk[NBLK];
 #pragma unroll
     for (int b = 0; b < NCT; ++b) {
-        if (b + 1 < NCT) load_frags(pc.q, b + 1, fq[(b + 1) & 1]);
+        if (b + 1 < NCT) load_frags(qc0, b + 1, fq[(b + 1) & 1]);
 #pragma unroll
         for (int jt = 0; jt <= b; ++jt) {
             f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
@@ -253,7 +258,7 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
             float val[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                val[i] = (jt < b || 4 * gq + i <= m) ? fast_exp(gr[b] - gc[i]) * acc[i] : 0.f;
+                val[i] = (jt < b || 4 * gq + i <= m) ? fast_exp(gr[b] - gc[i]) * (acc[i] * pc.scale) : 0.f;
             pk[bidx(b, jt)] = uint2{cvt_pk(val[0], val[1]), cvt_pk(val[2], val[3])};
         }
     }
@@ -351,16 +356,15 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
     //      released the previous chunk's (row 4 it + gq, segment m);
     //      chunk 0 was staged by the whole workgroup
     if (x == 0) return;
+    // (The zero stores before the loads are dead; without them the compiler
+    // kept these arrays in scratch memory across the waits below.)
     uint4 sk[SITEMS], sq[SITEMS];
 #pragma unroll
     for (int it = 0; it < SITEMS; ++it) {
-        const int r = 4 * it + gq;
+        const unsigned off = (unsigned)min(4 * it + gq, L - 1) * qks + 8u * m;
         sk[it] = sq[it] = uint4{0, 0, 0, 0};
-        if (r < L) {
-            const size_t tq = (size_t)(tb + r) * pc.qk_stride + (size_t)pc.hq * D + m * 8;
-            sk[it] = *reinterpret_cast<const uint4*>(pc.k + tq);
-            sq[it] = *reinterpret_cast<const uint4*>(pc.q + tq);
-        }
+        sk[it] = *reinterpret_cast<const uint4*>(kc0 + off);
+        sq[it] = *reinterpret_cast<const uint4*>(qc0 + off);
     }
     // K buffer x & 1 was last read by the update of chunk x - 2
     wait_ge(&sm.cnt[CNT_KFREE], (unsigned)(x >= 2 ? NS * (x - 1) : 0));
@@ -370,12 +374,12 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
 #pragma unroll
     for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.qb[4 * it + gq][m * 8]) = sq[it];
     signal(&sm.cnt[CNT_STG_KQ], lane);
+    const uint16_t* vc0 = pc.v + (size_t)tb * pc.v_stride + (size_t)pc.h * D;
     uint4 sv[SITEMS];
 #pragma unroll
     for (int it = 0; it < SITEMS; ++it) {
-        const int r = 4 * it + gq;
         sv[it] = uint4{0, 0, 0, 0};
-        if (r < L) sv[it] = *reinterpret_cast<const uint4*>(pc.v + (size_t)(tb + r) * pc.v_stride + (size_t)pc.h * D + m * 8);
+        sv[it] = *reinterpret_cast<const uint4*>(vc0 + (unsigned)min(4 * it + gq, L - 1) * (unsigned)pc.v_stride + 8u * m);
     }
     wait_ge(&sm.cnt[CNT_VFREE], (unsigned)(NS * x));
 #pragma unroll
@@ -437,6 +441,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
     if (wave < NS) {
         // ======================= state waves ===================================
         const int vcol0 = wave * VW;
+        const SplitMasks spm = split_masks();
         f32x4_t st[NDT][NVT];  // st[dt][vt][i] = S[v][d], v = vcol0 + 16 vt + m, d = 16 dt + 4 gq + i
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt)
@@ -460,13 +465,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             wait_ge(&sm.cnt[CNT_STG_KQ], (unsigned)(c + 1));
             // K S0^T (S0 hi + lo), rows t; (Q S0^T)^T (S0 hi), rows v
             f32x4_t ks[NCT][NVT], ot[NVT][NCT];
-#pragma unroll
-            for (int ct = 0; ct < NCT; ++ct)
-#pragma unroll
-                for (int vt = 0; vt < NVT; ++vt) {
-                    ks[ct][vt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-                    ot[vt][ct] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-                }
+            const f32x4_t zero4 = {0.f, 0.f, 0.f, 0.f};
             // Software pipeline over the contraction: the operands and the
             // hi/lo split of step kq + 1 are prepared while the products of
             // step kq run, interleaved by the scheduling groups below.
@@ -477,7 +476,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                 aq[0][ct] = lds_frag_perm<32>(&sm.qb[16 * ct + m][0], 0, gq);
             }
 #pragma unroll
-            for (int vt = 0; vt < NVT; ++vt) acc_frag<32>(st[0][vt], st[1][vt], bh[0][vt], bl[0][vt]);
+            for (int vt = 0; vt < NVT; ++vt) acc_frag(st[0][vt], st[1][vt], bh[0][vt], bl[0][vt], spm);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int kq = 0; kq < D / 32; ++kq) {
@@ -490,15 +489,15 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     }
 #pragma unroll
                     for (int vt = 0; vt < NVT; ++vt)
-                        acc_frag<32>(st[2 * kq + 2][vt], st[2 * kq + 3][vt], bh[cur ^ 1][vt], bl[cur ^ 1][vt]);
+                        acc_frag(st[2 * kq + 2][vt], st[2 * kq + 3][vt], bh[cur ^ 1][vt], bl[cur ^ 1][vt], spm);
                 }
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
                     for (int vt = 0; vt < NVT; ++vt) {
-                        ks[ct][vt] = mma(ak[cur][ct], bh[cur][vt], ks[ct][vt]);
+                        ks[ct][vt] = mma(ak[cur][ct], bh[cur][vt], kq == 0 ? zero4 : ks[ct][vt]);
                         ks[ct][vt] = mma(ak[cur][ct], bl[cur][vt], ks[ct][vt]);
-                        ot[vt][ct] = mma(bh[cur][vt], aq[cur][ct], ot[vt][ct]);
+                        ot[vt][ct] = mma(bh[cur][vt], aq[cur][ct], kq == 0 ? zero4 : ot[vt][ct]);
                     }
 #pragma unroll
                 for (int i = 0; i < 8; ++i) {
@@ -531,14 +530,14 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             f32x4_t uu[NCT][NVT];
             bf16x8_t wh[2][NVT], wl[2][NVT];
 #pragma unroll
-            for (int vt = 0; vt < NVT; ++vt) acc_frag<32>(ks[0][vt], ks[1][vt], wh[0][vt], wl[0][vt]);
+            for (int vt = 0; vt < NVT; ++vt) acc_frag(ks[0][vt], ks[1][vt], wh[0][vt], wl[0][vt], spm);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int kc = 0; kc < C; kc += 32) {
                 const int hb = kc / 32;
                 if (hb == 0) {
 #pragma unroll
-                    for (int vt = 0; vt < NVT; ++vt) acc_frag<32>(ks[2][vt], ks[3][vt], wh[1][vt], wl[1][vt]);
+                    for (int vt = 0; vt < NVT; ++vt) acc_frag(ks[2][vt], ks[3][vt], wh[1][vt], wl[1][vt], spm);
                 }
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) {
@@ -547,7 +546,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     const bf16x8_t al = blk_frag_t(sl.tl, sm.zero, ct, kc, m, gq);
 #pragma unroll
                     for (int vt = 0; vt < NVT; ++vt) {
-                        const f32x4_t u0 = (kc == 0) ? f32x4_t{0.f, 0.f, 0.f, 0.f} : uu[ct][vt];
+                        const f32x4_t u0 = (kc == 0) ? zero4 : uu[ct][vt];
                         uu[ct][vt] = mma(ah, wh[hb][vt], u0);
                         uu[ct][vt] = mma(ah, wl[hb][vt], uu[ct][vt]);
                         uu[ct][vt] = mma(al, wh[hb][vt], uu[ct][vt]);
@@ -574,7 +573,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             for (int hb = 0; hb < 2; ++hb)
 #pragma unroll
                 for (int vt = 0; vt < NVT; ++vt)
-                    acc_frag<32>(uu[2 * hb][vt] * eglv[2 * hb], uu[2 * hb + 1][vt] * eglv[2 * hb + 1], uth[hb][vt], utl[hb][vt]);
+                    acc_frag(uu[2 * hb][vt] * eglv[2 * hb], uu[2 * hb + 1][vt] * eglv[2 * hb + 1], uth[hb][vt], utl[hb][vt], spm);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int dt = 0; dt < NDT; ++dt) {
@@ -590,11 +589,11 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                 }
             }
             signal(&sm.cnt[CNT_KFREE], lane);
-            // O^T = diag(exp(gamma)) (Q S0^T)^T + U^T (M o Q K^T)^T  (U hi); its
-            // vector work overlaps the update's products
+            // scale O^T = scale diag(exp(gamma)) (Q S0^T)^T + U^T (scale M o Q K^T)^T
+            // (U hi); its vector work overlaps the update's products
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) {
-                const float e = sl.eg[16 * ct + m];
+                const float e = sl.eg[16 * ct + m] * scale;
 #pragma unroll
                 for (int vt = 0; vt < NVT; ++vt) ot[vt][ct] *= e;
             }
@@ -619,7 +618,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                 if (row < L) {
 #pragma unroll
                     for (int vt = 0; vt < NVT; ++vt) {
-                        const f32x4_t a = ot[vt][ct] * scale;
+                        const f32x4_t& a = ot[vt][ct];
                         const uint2 pk = {cvt_pk(a[0], a[1]), cvt_pk(a[2], a[3])};
                         *reinterpret_cast<uint2*>(o + (size_t)(t0 + row) * v_stride + (size_t)h * D + vcol0 +
                                                   16 * vt + 4 * gq) = pk;
@@ -637,7 +636,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             }
     } else {
         // ======================= producer waves ================================
-        const ProdCtx pc = {q, k, v, g, beta, qk_stride, v_stride, seq_beg, seq_len, hq, h, H_v, wave - NS};
+        const ProdCtx pc = {q, k, v, g, beta, qk_stride, v_stride, seq_beg, seq_len, hq, h, H_v, wave - NS, scale};
         for (int x = wave - NS, j = 0; x < nch; x += NP, ++j) {
             int mo = m, go = gq;
             asm volatile("" : "+v"(mo), "+v"(go));
