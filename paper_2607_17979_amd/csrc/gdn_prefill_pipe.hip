@@ -164,12 +164,24 @@ __device__ __forceinline__ bf16x8_t blk_frag_t(const uint16_t (*blocks)[16][16],
 // element i = X[4 g + i][m]) is the B operand of X and the A operand of X^T
 // (contraction index 4 g + i), so prod(acc(X), acc(Y)) = acc(X^T Y).
 
-// 16 x 16 x 16 product in fp32: four 16x16x4 fp32 MFMAs, step s contracting
-// indices 4 g + s.
-__device__ __forceinline__ f32x4_t prodf(const f32x4_t& a, const f32x4_t& b, f32x4_t acc) {
-#pragma unroll
-    for (int s = 0; s < 4; ++s) acc = mma_f32(a[s], b[s], acc);
-    return acc;
+// An accumulator-layout block split into bf16 hi and lo (four values per lane).
+struct Split16 {
+    uint2 h, l;
+};
+__device__ __forceinline__ Split16 split16(const f32x4_t& x) {
+    Split16 r;
+    split_pair(x[0], x[1], r.h.x, r.l.x);
+    split_pair(x[2], x[3], r.h.y, r.l.y);
+    return r;
+}
+// prod(acc(X), acc(Y)) = acc(X^T Y) on split bf16 operands: hi.hi, hi.lo and
+// lo.hi as three 16x16x16 MFMAs, each accumulating in fp32.  (Packing hi.hi
+// and hi.lo into one 16x16x32 MFMA lost the small terms within the
+// instruction's own sum and failed parity.)  Relative error about 2^-16.
+__device__ __forceinline__ f32x4_t prods(const Split16& a, const Split16& b, const f32x4_t& acc) {
+    f32x4_t t = mma(__builtin_bit_cast(s16x4_t, a.h), __builtin_bit_cast(s16x4_t, b.h), acc);
+    t = mma(__builtin_bit_cast(s16x4_t, a.h), __builtin_bit_cast(s16x4_t, b.l), t);
+    return mma(__builtin_bit_cast(s16x4_t, a.l), __builtin_bit_cast(s16x4_t, b.h), t);
 }
 
 __device__ __forceinline__ bf16x8_t as_frag(const uint4& u) { return __builtin_bit_cast(bf16x8_t, u); }
@@ -289,7 +301,7 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
     //      substitution in fp32, lane 16 b + j solving column j of
     //      block b (rows of N_b are read as LDS broadcasts); then block
     //      columns T_bJ = -D_b sum_{kb=J}^{b-1} A_{b,kb} T_{kb,J} (b > J)
-    //      on fp32 MFMA.
+    //      on split-bf16 MFMA.
     float* scb = scr + gq * 16 * SP;  // this lane's block b = gq
 #pragma unroll
     for (int b = 0; b < NCT; ++b)     // row m of N_b, columns 4 gq .. 4 gq + 3
@@ -326,15 +338,29 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
             for (int i = 0; i < 4; ++i) ddt[b][i] = -scr[(16 * b + 4 * gq + i) * SP + m];
         }
     }
+    {
+        // block-column sweep on split bf16 products; every operand is split once
+        const f32x4_t zero4 = {0.f, 0.f, 0.f, 0.f};
+        Split16 sat[NBLK], sdd[NCT - 1], sdt[NCT], stt[NBLK];
 #pragma unroll
-    for (int bi = 1; bi < NCT; ++bi)
+        for (int bi = 1; bi < NCT; ++bi) {
+            sdt[bi] = split16(ddt[bi]);
 #pragma unroll
-        for (int J = 0; J < bi; ++J) {
-            f32x4_t y = prodf(at[bidx(bi, J)], dd[J], f32x4_t{0.f, 0.f, 0.f, 0.f});
-#pragma unroll
-            for (int kb = J + 1; kb < bi; ++kb) y = prodf(at[bidx(bi, kb)], tt[bidx(kb, J)], y);
-            tt[bidx(bi, J)] = prodf(ddt[bi], y, f32x4_t{0.f, 0.f, 0.f, 0.f});
+            for (int kb = 0; kb < bi; ++kb) sat[bidx(bi, kb)] = split16(at[bidx(bi, kb)]);
         }
+#pragma unroll
+        for (int J = 0; J + 1 < NCT; ++J) sdd[J] = split16(dd[J]);
+#pragma unroll
+        for (int bi = 1; bi < NCT; ++bi)
+#pragma unroll
+            for (int J = 0; J < bi; ++J) {
+                f32x4_t y = prods(sat[bidx(bi, J)], sdd[J], zero4);
+#pragma unroll
+                for (int kb = J + 1; kb < bi; ++kb) y = prods(sat[bidx(bi, kb)], stt[bidx(kb, J)], y);
+                tt[bidx(bi, J)] = prods(sdt[bi], split16(y), zero4);
+                if (bi + 1 < NCT) stt[bidx(bi, J)] = split16(tt[bidx(bi, J)]);
+            }
+    }
     // ---- publish to the slot once the state waves are done with its
     //      previous chunk
     wait_ge(&sm.cnt[CNT_SFREE0 + pc.pw], (unsigned)(NS * j));
