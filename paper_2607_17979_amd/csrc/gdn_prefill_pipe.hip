@@ -502,7 +502,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                 aq[0][ct] = lds_frag_perm<32>(&sm.qb[16 * ct + m][0], 0, gq);
             }
 #pragma unroll
-            for (int vt = 0; vt < NVT; ++vt) acc_frag(st[0][vt], st[1][vt], bh[0][vt], bl[0][vt], spm);
+            for (int vt = 0; vt < NVT; ++vt) acc_frag<32>(st[0][vt], st[1][vt], bh[0][vt], bl[0][vt]);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int kq = 0; kq < D / 32; ++kq) {
@@ -515,7 +515,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     }
 #pragma unroll
                     for (int vt = 0; vt < NVT; ++vt)
-                        acc_frag(st[2 * kq + 2][vt], st[2 * kq + 3][vt], bh[cur ^ 1][vt], bl[cur ^ 1][vt], spm);
+                        acc_frag<32>(st[2 * kq + 2][vt], st[2 * kq + 3][vt], bh[cur ^ 1][vt], bl[cur ^ 1][vt]);
                 }
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct)
