@@ -413,15 +413,19 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
     signal(&sm.cnt[CNT_STG_V], lane);
 }
 
-// NS state waves (4 or 8), each owning D / NS value columns.
-template <int NS>
+// NS state waves, each owning NVT 16-wide tiles of value columns; a workgroup
+// covers NS * NVT * 16 of the D value columns of its head, so a head is split
+// over VSPLIT = D / (16 NS NVT) workgroups (each repeating the producer work of
+// the head), which spreads few long sequences over more compute units.
+template <int NS, int NVT>
 __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const float* __restrict__ g, const float* __restrict__ beta, const int32_t* __restrict__ cu,
     const int32_t* __restrict__ order, const float* initial_state, float* final_state,
     uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale) {
-    constexpr int VW = D / NS;          // value columns per state wave
-    constexpr int NVT = VW / 16;        // 16-wide value tiles per state wave
+    constexpr int VW = 16 * NVT;        // value columns per state wave
+    constexpr int VSPLIT = D / (NS * VW);
+    static_assert(VSPLIT * NS * VW == D, "value columns must tile D");
     __shared__ Smem sm;
 
     const int tid = threadIdx.x;
@@ -430,9 +434,11 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
     const int m = lane & 15;
     const int gq = lane >> 4;
 
-    const int item = logical_item(blockIdx.x, N * H_v);
-    const int rank = item / H_v;
-    const int h = item - rank * H_v;
+    const int item = logical_item(blockIdx.x, N * H_v * VSPLIT);
+    const int head_item = item / VSPLIT;
+    const int vblock = item - head_item * VSPLIT;
+    const int rank = head_item / H_v;
+    const int h = head_item - rank * H_v;
     const int n = order[rank];
     const int hq = h / (H_v / H_qk);
     const int seq_beg = cu[n];
@@ -466,7 +472,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
 
     if (wave < NS) {
         // ======================= state waves ===================================
-        const int vcol0 = wave * VW;
+        const int vcol0 = (vblock * NS + wave) * VW;
         const SplitMasks spm = split_masks();
         f32x4_t st[NDT][NVT];  // st[dt][vt][i] = S[v][d], v = vcol0 + 16 vt + m, d = 16 dt + 4 gq + i
 #pragma unroll
@@ -673,17 +679,37 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
 
 }  // namespace pipe
 
-#ifndef GDN_PIPE_STATE_WAVES
-#define GDN_PIPE_STATE_WAVES 4
-#endif
+// Compute units of the current device (queried once per device).
+static int compute_units() {
+    static int cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
+    if (dev < 64 && cache[dev] > 0) return cache[dev];
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    if (dev < 64) cache[dev] = n;
+    return n;
+}
 
-hipError_t launch_prefill_pipe(const PrefillArgs& a, const int32_t* order, hipStream_t stream) {
-    constexpr int NS = GDN_PIPE_STATE_WAVES;
-    hipLaunchKernelGGL(pipe::prefill_pipe_kernel<NS>, dim3((unsigned)(a.N * a.H_v)), dim3(64 * (NS + pipe::NP)),
-                       0, stream, (const uint16_t*)a.q, (const uint16_t*)a.k, (const uint16_t*)a.v, a.g,
-                       a.beta, a.cu_seqlens, order, a.initial_state, a.final_state, (uint16_t*)a.o,
-                       a.N, a.H_qk, a.H_v, a.scale);
+template <int NS, int NVT>
+static hipError_t launch_pipe(const PrefillArgs& a, const int32_t* order, hipStream_t stream) {
+    constexpr int VSPLIT = pipe::D / (16 * NS * NVT);
+    hipLaunchKernelGGL((pipe::prefill_pipe_kernel<NS, NVT>), dim3((unsigned)(a.N * a.H_v * VSPLIT)),
+                       dim3(64 * (NS + pipe::NP)), 0, stream, (const uint16_t*)a.q, (const uint16_t*)a.k,
+                       (const uint16_t*)a.v, a.g, a.beta, a.cu_seqlens, order, a.initial_state, a.final_state,
+                       (uint16_t*)a.o, a.N, a.H_qk, a.H_v, a.scale);
     return hipGetLastError();
+}
+
+// One workgroup per (sequence, head) when there are enough of them to fill the
+// device; otherwise each head's value columns are split over 2 or 4
+// workgroups (one workgroup per compute unit fits in LDS).
+hipError_t launch_prefill_pipe(const PrefillArgs& a, const int32_t* order, hipStream_t stream) {
+    const long heads = (long)a.N * a.H_v;
+    const long cus = compute_units();
+    if (heads * 4 <= cus) return launch_pipe<2, 1>(a, order, stream);
+    if (heads * 2 <= cus) return launch_pipe<4, 1>(a, order, stream);
+    return launch_pipe<4, 2>(a, order, stream);
 }
 
 }  // namespace gdn

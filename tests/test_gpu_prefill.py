@@ -186,3 +186,30 @@ def test_prefill_then_decode_continues_the_sequence():
                                       full.initial_state)
     check_outputs(np.concatenate(outs), o_ref, "prefill+decode")
     check_states(fin.cpu().numpy(), s_ref, "prefill+decode")
+
+
+def test_prefill_value_split_is_bitwise_batch_independent():
+    """With few (sequence, head) items the kernel splits each head's value
+    columns over 2 or 4 workgroups (1 x 32 heads: 4-way; 3 x 32: 2-way on
+    256 compute units; 8 x 32: none).  Every value column evolves on its own,
+    so one sequence gives bitwise the same outputs and final state in all
+    three batches; the single-sequence run is also checked against the oracle."""
+    import torch
+
+    dev = device()
+    L, H_qk, H_v, D = 200, 16, 32, 128
+    base = wl.prefill_inputs(41, [L], H_qk, H_v, D, state_std=0.02, scale=D ** -0.5)
+    o1, f1 = _prefill_gpu(base, dev)
+    _full_oracle_check(base, o1, f1, "value split, 1 sequence")
+    for copies in (3, 8):
+        note(f"prefill value split: {copies} copies of one {L}-token sequence")
+        rep = wl.PrefillInputs(
+            q=np.concatenate([base.q] * copies), k=np.concatenate([base.k] * copies),
+            v=np.concatenate([base.v] * copies), g=np.concatenate([base.g] * copies),
+            beta=np.concatenate([base.beta] * copies),
+            cu_seqlens=np.arange(copies + 1, dtype=np.int32) * L,
+            initial_state=np.concatenate([base.initial_state] * copies), scale=base.scale)
+        o, f = _prefill_gpu(rep, dev)
+        for c in range(copies):
+            assert torch.equal(o[c * L:(c + 1) * L].view(torch.int16), o1.view(torch.int16)), (copies, c)
+            assert torch.equal(f[c].view(torch.int32), f1[0].view(torch.int32)), (copies, c)
