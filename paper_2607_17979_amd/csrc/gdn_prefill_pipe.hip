@@ -56,14 +56,11 @@ struct Slot {
 };
 
 enum {
-    CNT_STG_KQ = 0,   // chunks whose K and Q rows are staged
-    CNT_STG_V,        // chunks whose V rows are staged
-    CNT_KFREE,        // state-wave releases of a K row buffer (after the update)
-    CNT_QFREE,        // state-wave releases of the Q row buffer
-    CNT_VFREE,        // state-wave releases of the V row buffer
+    CNT_STG = 0,      // chunks whose K, Q and V rows are staged
+    CNT_QVFREE,       // state-wave releases of the Q and V row buffers (after W)
+    CNT_DONE,         // state-wave chunk completions: the chunk's K buffer and slot are free
     CNT_READY0,       // + p: chunks written to slot p
-    CNT_SFREE0 = CNT_READY0 + NP,  // + p: state-wave releases of slot p
-    NCNT = CNT_SFREE0 + NP
+    NCNT = CNT_READY0 + NP
 };
 
 struct Smem {
@@ -363,7 +360,7 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
     }
     // ---- publish to the slot once the state waves are done with its
     //      previous chunk
-    wait_ge(&sm.cnt[CNT_SFREE0 + pc.pw], (unsigned)(NS * j));
+    wait_ge(&sm.cnt[CNT_DONE], (unsigned)(x >= 4 ? NS * (x - 3) : 0));   // chunk x - 4 done
 #pragma unroll
     for (int b = 0; b < NCT; ++b)
 #pragma unroll
@@ -393,13 +390,12 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
         sq[it] = *reinterpret_cast<const uint4*>(qc0 + off);
     }
     // K buffer x & 1 was last read by the update of chunk x - 2
-    wait_ge(&sm.cnt[CNT_KFREE], (unsigned)(x >= 2 ? NS * (x - 1) : 0));
+    wait_ge(&sm.cnt[CNT_DONE], (unsigned)(x >= 2 ? NS * (x - 1) : 0));
 #pragma unroll
     for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.kb[x & 1][4 * it + gq][m * 8]) = sk[it];
-    wait_ge(&sm.cnt[CNT_QFREE], (unsigned)(NS * x));
+    wait_ge(&sm.cnt[CNT_QVFREE], (unsigned)(NS * x));
 #pragma unroll
     for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.qb[4 * it + gq][m * 8]) = sq[it];
-    signal(&sm.cnt[CNT_STG_KQ], lane);
     const uint16_t* vc0 = pc.v + (size_t)tb * pc.v_stride + (size_t)pc.h * D;
     uint4 sv[SITEMS];
 #pragma unroll
@@ -407,10 +403,9 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
         sv[it] = uint4{0, 0, 0, 0};
         sv[it] = *reinterpret_cast<const uint4*>(vc0 + (unsigned)min(4 * it + gq, L - 1) * (unsigned)pc.v_stride + 8u * m);
     }
-    wait_ge(&sm.cnt[CNT_VFREE], (unsigned)(NS * x));
 #pragma unroll
     for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.vb[4 * it + gq][m * 8]) = sv[it];
-    signal(&sm.cnt[CNT_STG_V], lane);
+    signal(&sm.cnt[CNT_STG], lane);
 }
 
 // NS state waves, each owning NVT 16-wide tiles of value columns; a workgroup
@@ -450,7 +445,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
 
     // Every wave stages chunk 0's K, Q, V rows before the roles split, so the
     // state waves can start on it while producer 0 prepares the rest.
-    if (tid < NCNT) sm.cnt[tid] = (tid == CNT_STG_KQ || tid == CNT_STG_V) && nch > 0 ? 1u : 0u;
+    if (tid < NCNT) sm.cnt[tid] = (tid == CNT_STG && nch > 0) ? 1u : 0u;
     for (int i = tid; i < 16 * 16; i += 64 * (NS + NP)) (&sm.zero[0][0])[i] = 0;
     if (nch > 0) {
         const int L0 = min(C, seq_len);
@@ -494,7 +489,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             const int t0 = seq_beg + c * C;
             const Slot& sl = sm.slot[c % NP];
             const uint16_t (*kb)[PD] = sm.kb[par];
-            wait_ge(&sm.cnt[CNT_STG_KQ], (unsigned)(c + 1));
+            wait_ge(&sm.cnt[CNT_STG], (unsigned)(c + 1));
             // K S0^T (S0 hi + lo), rows t; (Q S0^T)^T (S0 hi), rows v
             f32x4_t ks[NCT][NVT], ot[NVT][NCT];
             const f32x4_t zero4 = {0.f, 0.f, 0.f, 0.f};
@@ -538,10 +533,8 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   // VALU
                 }
             }
-            signal(&sm.cnt[CNT_QFREE], lane);
             // W = V - diag(exp(gamma)) K S0^T (in ks)
             wait_ge(&sm.cnt[CNT_READY0 + c % NP], (unsigned)(c / NP + 1));
-            wait_ge(&sm.cnt[CNT_STG_V], (unsigned)(c + 1));
             f32x4_t egr[NCT];
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) egr[ct] = *reinterpret_cast<const f32x4_t*>(&sl.eg[16 * ct + 4 * gq]);
@@ -556,7 +549,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
 #pragma unroll
                     for (int i = 0; i < 4; ++i) ks[ct][vt][i] = fmaf(-egr[ct][i], ks[ct][vt][i], vf[i]);
                 }
-            signal(&sm.cnt[CNT_VFREE], lane);
+            signal(&sm.cnt[CNT_QVFREE], lane);
             // U = T diag(beta) W  (hi*hi + hi*lo + lo*hi); the split of the
             // second half of W overlaps the products of the first.
             f32x4_t uu[NCT][NVT];
@@ -620,7 +613,6 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     st[dt][vt] = mma(a1, utl[1][vt], st[dt][vt]);
                 }
             }
-            signal(&sm.cnt[CNT_KFREE], lane);
             // scale O^T = scale diag(exp(gamma)) (Q S0^T)^T + U^T (scale M o Q K^T)^T
             // (U hi); its vector work overlaps the update's products
 #pragma unroll
@@ -642,7 +634,8 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     for (int vt = 0; vt < NVT; ++vt) ot[vt][ct] = mma(uh[vt], bp, ot[vt][ct]);
                 }
             }
-            signal(&sm.cnt[CNT_SFREE0 + c % NP], lane);
+            // all LDS reads of chunk c are done: its K buffer and result slot are free
+            signal(&sm.cnt[CNT_DONE], lane);
             // Outputs: lane m + 16 gq holds token 16 ct + m, value columns 4 gq .. 4 gq + 3.
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) {
