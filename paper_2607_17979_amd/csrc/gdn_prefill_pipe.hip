@@ -493,9 +493,10 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             // K S0^T (S0 hi + lo), rows t; (Q S0^T)^T (S0 hi), rows v
             f32x4_t ks[NCT][NVT], ot[NVT][NCT];
             const f32x4_t zero4 = {0.f, 0.f, 0.f, 0.f};
-            // Software pipeline over the contraction: the operands and the
-            // hi/lo split of step kq + 1 are prepared while the products of
-            // step kq run, interleaved by the scheduling groups below.
+            // Software pipeline over the contraction: the operand reads of step
+            // kq + 1 are issued ahead of the products of step kq (the barrier
+            // keeps the scheduler from sinking them towards their use), and
+            // the hi/lo split of step kq + 1 is interleaved with those products.
             bf16x8_t ak[2][NCT], aq[2][NCT], bh[2][NVT], bl[2][NVT];
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) {
@@ -514,6 +515,9 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                         ak[cur ^ 1][ct] = lds_frag_perm<32>(&kb[16 * ct + m][0], 32 * (kq + 1), gq);
                         aq[cur ^ 1][ct] = lds_frag_perm<32>(&sm.qb[16 * ct + m][0], 32 * (kq + 1), gq);
                     }
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                if (kq + 1 < D / 32) {
 #pragma unroll
                     for (int vt = 0; vt < NVT; ++vt)
                         acc_frag<32>(st[2 * kq + 2][vt], st[2 * kq + 3][vt], bh[cur ^ 1][vt], bl[cur ^ 1][vt]);
@@ -527,14 +531,25 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                         ot[vt][ct] = mma(bh[cur][vt], aq[cur][ct], kq == 0 ? zero4 : ot[vt][ct]);
                     }
 #pragma unroll
-                for (int i = 0; i < 8; ++i) {
+                for (int i = 0; i < 4 * NVT; ++i) {
                     __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);   // MFMA
-                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
                     __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   // VALU
                 }
+                __builtin_amdgcn_sched_barrier(0);
             }
             // W = V - diag(exp(gamma)) K S0^T (in ks)
             wait_ge(&sm.cnt[CNT_READY0 + c % NP], (unsigned)(c / NP + 1));
+            // T operands of U = T diag(beta) W, read now so that their latency
+            // hides behind the vector work of W
+            bf16x8_t tah[NCT][2], tal[NCT][2];
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                for (int hb = 0; hb < 2; ++hb) {
+                    if (32 * hb > 16 * ct + 15) continue;
+                    tah[ct][hb] = blk_frag_t(sl.th, sm.zero, ct, 32 * hb, m, gq);
+                    tal[ct][hb] = blk_frag_t(sl.tl, sm.zero, ct, 32 * hb, m, gq);
+                }
             f32x4_t egr[NCT];
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) egr[ct] = *reinterpret_cast<const f32x4_t*>(&sl.eg[16 * ct + 4 * gq]);
@@ -567,8 +582,8 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) {
                     if (kc > 16 * ct + 15) continue;
-                    const bf16x8_t ah = blk_frag_t(sl.th, sm.zero, ct, kc, m, gq);
-                    const bf16x8_t al = blk_frag_t(sl.tl, sm.zero, ct, kc, m, gq);
+                    const bf16x8_t& ah = tah[ct][hb];
+                    const bf16x8_t& al = tal[ct][hb];
 #pragma unroll
                     for (int vt = 0; vt < NVT; ++vt) {
                         const f32x4_t u0 = (kc == 0) ? zero4 : uu[ct][vt];
@@ -579,9 +594,8 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                 }
                 if (hb == 0) {
 #pragma unroll
-                    for (int i = 0; i < 8; ++i) {
+                    for (int i = 0; i < 4 * NVT; ++i) {
                         __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);   // MFMA
-                        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
                         __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   // VALU
                     }
                 }
@@ -593,6 +607,15 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) eglv[ct] = *reinterpret_cast<const f32x4_t*>(&sl.egl[16 * ct + 4 * gq]);
             const float eg_last = sl.eg[C - 1];
+            // P operands of the output products, read ahead of the update
+            bf16x8_t pf[NCT][2];
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                for (int hb = 0; hb < 2; ++hb) {
+                    if (32 * hb > 16 * ct + 15) continue;
+                    pf[ct][hb] = blk_frag(sl.pm, sm.zero, ct, 32 * hb, m, gq);
+                }
             bf16x8_t uth[2][NVT], utl[2][NVT];
 #pragma unroll
             for (int hb = 0; hb < 2; ++hb)
@@ -629,7 +652,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) {
                     if (kc > 16 * ct + 15) continue;
-                    const bf16x8_t bp = blk_frag(sl.pm, sm.zero, ct, kc, m, gq);
+                    const bf16x8_t& bp = pf[ct][kc / 32];
 #pragma unroll
                     for (int vt = 0; vt < NVT; ++vt) ot[vt][ct] = mma(uh[vt], bp, ot[vt][ct]);
                 }
