@@ -97,13 +97,16 @@ class Decode:
     served from the last-level cache and the event pair around the call
     amortises its own overhead."""
 
-    def __init__(self, dev, B, H_qk, H_v, D, seed, nbuf, per_step=1):
+    def __init__(self, dev, B, H_qk, H_v, D, seed, nbuf, per_step=1, n_inputs=1):
         import torch
         from paper_2607_17979_amd import workloads as wl
 
         self.B, self.H_qk, self.H_v, self.D = B, H_qk, H_v, D
         self.host = wl.decode_inputs(seed, B, H_qk, H_v, D)
-        self.x = _dev_inputs_decode(self.host, dev)
+        # launch i takes input set i % n_inputs (fresh q, k, v, g, beta per step)
+        self.xs = [_dev_inputs_decode(self.host, dev)] + [
+            _dev_inputs_decode(wl.decode_step_inputs(seed, s, B, H_qk, H_v, D), dev)
+            for s in range(1, n_inputs)]
         self.states = [wl.to_torch(self.host.state, dev) for _ in range(nbuf)]
         self.o = torch.empty((B, H_v, D), dtype=torch.bfloat16, device=dev)
         self.i = 0
@@ -113,8 +116,8 @@ class Decode:
     def __call__(self):
         from paper_2607_17979_amd import gdn
 
-        x = self.x
         for _ in range(self.per_step):
+            x = self.xs[self.i % len(self.xs)]
             gdn.gdn_decode(x["q"], x["k"], x["v"], x["g"], x["beta"],
                            self.states[self.i % len(self.states)], self.o)
             self.i += 1
@@ -169,6 +172,38 @@ def _time_parts(parts, steps, warmup):
     per = [sum(evs[s][j][0].elapsed_time(evs[s][j][1]) for s in range(steps)) / steps
            for j in range(len(parts))]
     return wall * 1e3 / steps, per
+
+
+def _time_graph(fn, launches, replays, warmup):
+    """Capture ``launches`` calls of ``fn`` in one HIP graph and time ``replays``
+    replays with HIP events on the replay stream; returns the median ms per
+    call.  Removes the host's per-launch cost, which dominates for small decode
+    batches."""
+    import statistics
+    import torch
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for _ in range(warmup):
+            fn()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(launches):
+            fn()
+    graph.replay()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(replays):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    return statistics.median(ts) / launches
 
 
 def _cpu_baseline_decode(dec, budget_s=10.0):
@@ -282,16 +317,22 @@ def main(argv=None):
         lines = []
         for B in batches:
             nbuf = max(1, min(4, (512 << 20) // (B * w["H_v"] * w["D"] * w["D"] * 4)))
-            d = Decode(dev, B, w["H_qk"], w["H_v"], w["D"], w["seed"] + B, nbuf=nbuf)
-            ms_step, per = _time_parts([d], w["steps"], args.warmup)
-            gbs = d.bytes / (per[0] * 1e-3) / 1e9
-            lines.append(dict(batch=B, us_per_step=per[0] * 1e3, GBs=gbs, frac=gbs / HBM_PEAK_GBS,
-                              state_buffers=nbuf))
-            print(f"# decode B={B}: {per[0]*1e3:.2f} us/step, {gbs:.1f} GB/s", file=sys.stderr, flush=True)
+            d = Decode(dev, B, w["H_qk"], w["H_v"], w["D"], w["seed"] + B, nbuf=nbuf, n_inputs=8)
+            # eager: one host launch per step, HIP events around each
+            _, per = _time_parts([d], w["steps"], args.warmup)
+            # graph: the steps captured once and replayed (the kernel without host launch cost)
+            ms_graph = _time_graph(d, w["steps"], 5, args.warmup)
+            gbs = d.bytes / (ms_graph * 1e-3) / 1e9
+            lines.append(dict(batch=B, us_per_step=ms_graph * 1e3, GBs=gbs, frac=gbs / HBM_PEAK_GBS,
+                              us_per_step_eager=per[0] * 1e3,
+                              GBs_eager=d.bytes / (per[0] * 1e-3) / 1e9, state_buffers=nbuf))
+            print(f"# decode B={B}: graph {ms_graph*1e3:.2f} us/step ({gbs:.1f} GB/s); "
+                  f"eager {per[0]*1e3:.2f} us/step", file=sys.stderr, flush=True)
         big = lines[-1]
         out.update(value=big["GBs"], unit="GB/s", ms_per_step=big["us_per_step"] / 1e3,
                    steps=w["steps"], dtype="f32",
-                   config=dict(workload=f"decode sweep, batches {batches} x {w['steps']} steps, "
+                   config=dict(workload=f"decode sweep, batches {batches} x {w['steps']} steps "
+                                        f"(captured in a HIP graph, replayed), "
                                         f"H_v={w['H_v']}/H_qk={w['H_qk']}, d={w['D']}",
                                sweep=lines),
                    roofline=dict(bound="hbm", achieved=big["GBs"], peak=HBM_PEAK_GBS, unit="GB/s",

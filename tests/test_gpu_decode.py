@@ -191,3 +191,50 @@ def test_decode_zero_batch():
     zs = torch.empty((0, 4, 128, 128), dtype=torch.float32, device=dev)
     gdn.gdn_decode(z, z, zv, zf, zf, zs, zv.clone())
     torch.cuda.synchronize()
+
+
+def test_decode_graph_replay_matches_eager():
+    """Decode steps captured once in a HIP graph and replayed three times, with
+    eager steps and synchronisations between the replays, leave bitwise the
+    states and outputs of the same steps run eagerly (the benchmark's decode
+    sweep times such replays)."""
+    import torch
+
+    dev = device()
+    B, H_qk, H_v, D, n, seed = 8, 16, 32, 128, 6, 31
+    note(f"decode graph replay: B={B}, {n} steps per replay, 3 replays")
+    xs = []
+    for s in range(n):
+        st = wl.decode_step_inputs(seed, s, B, H_qk, H_v, D)
+        xs.append(dict(q=to_dev(st.q, dev, bf16=True), k=to_dev(st.k, dev, bf16=True),
+                       v=to_dev(st.v, dev, bf16=True), g=to_dev(st.g, dev), b=to_dev(st.beta, dev)))
+    state0 = wl.decode_state(seed, B, H_v, D, 0.02)
+
+    def outs():
+        return [torch.empty((B, H_v, D), dtype=torch.bfloat16, device=dev) for _ in range(n)]
+
+    def run(state, os_):
+        for x, o in zip(xs, os_):
+            gdn.gdn_decode(x["q"], x["k"], x["v"], x["g"], x["b"], state, o)
+
+    s_graph, o_graph = to_dev(state0, dev), outs()
+    s_eager, o_eager = to_dev(state0, dev), outs()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run(to_dev(state0, dev), outs())          # warm-up before capture
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        run(s_graph, o_graph)
+    torch.cuda.synchronize()
+    assert torch.equal(s_graph, to_dev(state0, dev)), "capture must not execute the steps"
+    for r in range(3):
+        graph.replay()
+        torch.cuda.synchronize()
+        run(s_eager, o_eager)
+        torch.cuda.synchronize()
+        assert torch.equal(s_graph, s_eager), f"state after replay {r}"
+        for i, (a, b) in enumerate(zip(o_graph, o_eager)):
+            assert torch.equal(a, b), f"output of step {i} after replay {r}"
