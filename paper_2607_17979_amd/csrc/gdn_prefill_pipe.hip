@@ -659,19 +659,33 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             }
             // all LDS reads of chunk c are done: its K buffer and result slot are free
             signal(&sm.cnt[CNT_DONE], lane);
-            // Outputs: lane m + 16 gq holds token 16 ct + m, value columns 4 gq .. 4 gq + 3.
+            // Outputs: lane m + 16 gq holds, in ot[vt][ct], token 16 ct + m and
+            // value columns 16 vt + 4 gq .. + 3.  Two such tiles x, y are merged
+            // by a swap between lane groups gq and gq ^ 1 (v_permlane16_swap:
+            // group 2i ends with x of groups 2i, 2i + 1, group 2i + 1 with y of
+            // both), so that each lane stores 8 consecutive columns (16 bytes):
+            // x, y are the two value tiles when NVT is even, else token blocks
+            // ct and ct + 1.
+            const int odd = gq & 1, half = gq >> 1;
+            auto store_pair = [&](const f32x4_t& x, const f32x4_t& y, int row, int col) {
+                const auto p0 = __builtin_amdgcn_permlane16_swap(cvt_pk(x[0], x[1]), cvt_pk(y[0], y[1]), false, false);
+                const auto p1 = __builtin_amdgcn_permlane16_swap(cvt_pk(x[2], x[3]), cvt_pk(y[2], y[3]), false, false);
+                const uint4 pk = {p0[0], p1[0], p0[1], p1[1]};
+                if (row < L)
+                    *reinterpret_cast<uint4*>(o + (size_t)(t0 + row) * v_stride + (size_t)h * D + vcol0 + col) = pk;
+            };
+            if constexpr (NVT % 2 == 0) {
 #pragma unroll
-            for (int ct = 0; ct < NCT; ++ct) {
-                const int row = 16 * ct + m;
-                if (row < L) {
+                for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-                    for (int vt = 0; vt < NVT; ++vt) {
-                        const f32x4_t& a = ot[vt][ct];
-                        const uint2 pk = {cvt_pk(a[0], a[1]), cvt_pk(a[2], a[3])};
-                        *reinterpret_cast<uint2*>(o + (size_t)(t0 + row) * v_stride + (size_t)h * D + vcol0 +
-                                                  16 * vt + 4 * gq) = pk;
-                    }
-                }
+                    for (int vt = 0; vt < NVT; vt += 2)
+                        store_pair(ot[vt][ct], ot[vt + 1][ct], 16 * ct + m, 16 * vt + 16 * odd + 8 * half);
+            } else {
+#pragma unroll
+                for (int ct = 0; ct < NCT; ct += 2)
+#pragma unroll
+                    for (int vt = 0; vt < NVT; ++vt)
+                        store_pair(ot[vt][ct], ot[vt][ct + 1], 16 * (ct + odd) + m, 16 * vt + 8 * half);
             }
         }
 #pragma unroll
