@@ -37,7 +37,17 @@ namespace pipe {
 constexpr int D = 128, C = 64;
 constexpr int NP = 4;                 // producer waves = result slots
 constexpr int NDT = D / 16, NCT = C / 16;
-constexpr int PD = D + 8;             // LDS pitch (bf16) of [C][D] arrays
+// LDS pitch (bf16) of the [C][D] row buffers: 72 dwords, so eight
+// consecutive rows start 8 banks apart.  Columns are stored swizzled,
+// column c of row r at c ^ (r & 8) (8-byte units stay whole): the transposed
+// reads (8 consecutive rows x 4 eight-byte units per half wave) and the row
+// reads (16 rows x 2 units per half wave, rows r and r + 8 now 4 banks apart)
+// both touch 64 distinct banks.
+constexpr int PD = D + 16;
+// Swizzled column of row r of a row buffer or a P block.  Only bit 3 of the
+// column changes, so for c = c16 + c_lane with c16 a multiple of 16 the
+// swizzle applies to c_lane alone and c16 stays an address immediate.
+__device__ __forceinline__ int swz(int r, int c) { return c ^ (r & 8); }
 constexpr int NBLK = NCT * (NCT + 1) / 2;   // lower-triangular 16 x 16 blocks (10)
 constexpr int SEGS = D / 8;                 // 16-byte segments per q/k/v row
 constexpr int SITEMS = C * SEGS / 64;       // staged segments per producer lane (16)
@@ -114,8 +124,8 @@ __device__ __forceinline__ void wait_ge(unsigned* ctr, unsigned target) {
 __device__ __forceinline__ bf16x8_t blk_frag(const uint16_t (*blocks)[16][16], const uint16_t (*zero)[16],
                                              int ct, int kc, int m, int g) {
     const int j0 = kc >> 4;
-    const uint16_t* p0 = &blocks[bidx(ct, j0)][m][4 * g];
-    const uint16_t* p1 = (j0 + 1 <= ct) ? &blocks[bidx(ct, j0 + 1)][m][4 * g] : &zero[m][4 * g];
+    const uint16_t* p0 = &blocks[bidx(ct, j0)][m][swz(m, 4 * g)];
+    const uint16_t* p1 = (j0 + 1 <= ct) ? &blocks[bidx(ct, j0 + 1)][m][swz(m, 4 * g)] : &zero[m][4 * g];
     const uint2 lo = *reinterpret_cast<const uint2*>(p0);
     const uint2 hi = *reinterpret_cast<const uint2*>(p1);
     uint4 u = {lo.x, lo.y, hi.x, hi.y};
@@ -134,12 +144,14 @@ __device__ __forceinline__ uint2 lds_tr4(const uint16_t* p) {
     return __builtin_bit_cast(uint2, r);
 }
 
-// A operand whose rows are columns c0..c0+15 of a row-major [row][col] bf16
-// array, contraction over rows r0..r0+31 in the permuted order (slot j < 4:
-// row r0 + 4 g + j; slot j >= 4: row r0 + 16 + 4 g + (j - 4)).
+// A operand whose rows are columns c0..c0+15 (c0 a multiple of 16) of a
+// swizzled row buffer, contraction over rows r0..r0+31 (r0 a multiple of 16)
+// in the permuted order (slot j < 4: row r0 + 4 g + j; slot j >= 4: row
+// r0 + 16 + 4 g + (j - 4)).
 __device__ __forceinline__ bf16x8_t lds_frag_tr(const uint16_t (*a)[PD], int r0, int c0, int m, int g) {
-    const uint2 lo = lds_tr4(&a[r0 + 4 * g + (m >> 2)][c0 + 4 * (m & 3)]);
-    const uint2 hi = lds_tr4(&a[r0 + 16 + 4 * g + (m >> 2)][c0 + 4 * (m & 3)]);
+    const int r = 4 * g + (m >> 2), cl = swz(r, 4 * (m & 3));
+    const uint2 lo = lds_tr4(&a[r0 + r][c0 + cl]);
+    const uint2 hi = lds_tr4(&a[r0 + 16 + r][c0 + cl]);
     uint4 u = {lo.x, lo.y, hi.x, hi.y};
     return __builtin_bit_cast(bf16x8_t, u);
 }
@@ -205,6 +217,17 @@ struct ProdCtx {
     int seq_beg, seq_len, hq, h, H_v, pw;
     float scale;
 };
+
+// A/B operand from row r of a swizzled row buffer, contraction columns
+// k0..k0+31 (k0 a multiple of 32) in the permuted order of the accumulator
+// tiles (slot j < 4: column k0 + 4 g + j, slot j >= 4: k0 + 16 + 4 g + j - 4).
+__device__ __forceinline__ bf16x8_t row_frag(const uint16_t (*a)[PD], int r, int k0, int g) {
+    const int cl = swz(r, 4 * g);
+    const uint2 lo = *reinterpret_cast<const uint2*>(&a[r][k0 + cl]);
+    const uint2 hi = *reinterpret_cast<const uint2*>(&a[r][k0 + 16 + cl]);
+    uint4 u = {lo.x, lo.y, hi.x, hi.y};
+    return __builtin_bit_cast(bf16x8_t, u);
+}
 
 // Producer work for chunk x (the j-th chunk of producer pc.pw).  The lane
 // indices m, gq are passed in per chunk (opaque to the compiler), so the
@@ -365,7 +388,7 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
     for (int b = 0; b < NCT; ++b)
 #pragma unroll
         for (int jt = 0; jt <= b; ++jt)
-            *reinterpret_cast<uint2*>(&sl.pm[bidx(b, jt)][m][4 * gq]) = pk[bidx(b, jt)];
+            *reinterpret_cast<uint2*>(&sl.pm[bidx(b, jt)][m][swz(m, 4 * gq)]) = pk[bidx(b, jt)];
 #pragma unroll
     for (int b = 0; b < NCT; ++b) {
         store_split_t(sl.th[bidx(b, b)], sl.tl[bidx(b, b)], dd[b], br[b], m, gq);
@@ -392,10 +415,10 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
     // K buffer x & 1 was last read by the update of chunk x - 2
     wait_ge(&sm.cnt[CNT_DONE], (unsigned)(x >= 2 ? NS * (x - 1) : 0));
 #pragma unroll
-    for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.kb[x & 1][4 * it + gq][m * 8]) = sk[it];
+    for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.kb[x & 1][4 * it + gq][swz(4 * it + gq, m * 8)]) = sk[it];
     wait_ge(&sm.cnt[CNT_QVFREE], (unsigned)(NS * x));
 #pragma unroll
-    for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.qb[4 * it + gq][m * 8]) = sq[it];
+    for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.qb[4 * it + gq][swz(4 * it + gq, m * 8)]) = sq[it];
     const uint16_t* vc0 = pc.v + (size_t)tb * pc.v_stride + (size_t)pc.h * D;
     uint4 sv[SITEMS];
 #pragma unroll
@@ -404,7 +427,7 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
         sv[it] = *reinterpret_cast<const uint4*>(vc0 + (unsigned)min(4 * it + gq, L - 1) * (unsigned)pc.v_stride + 8u * m);
     }
 #pragma unroll
-    for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.vb[4 * it + gq][m * 8]) = sv[it];
+    for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.vb[4 * it + gq][swz(4 * it + gq, m * 8)]) = sv[it];
     signal(&sm.cnt[CNT_STG], lane);
 }
 
@@ -458,9 +481,9 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                 rq = *reinterpret_cast<const uint4*>(q + tq);
                 rv = *reinterpret_cast<const uint4*>(v + (size_t)(seq_beg + r) * v_stride + (size_t)h * D + seg * 8);
             }
-            *reinterpret_cast<uint4*>(&sm.kb[0][r][seg * 8]) = rk;
-            *reinterpret_cast<uint4*>(&sm.qb[r][seg * 8]) = rq;
-            *reinterpret_cast<uint4*>(&sm.vb[r][seg * 8]) = rv;
+            *reinterpret_cast<uint4*>(&sm.kb[0][r][swz(r, seg * 8)]) = rk;
+            *reinterpret_cast<uint4*>(&sm.qb[r][swz(r, seg * 8)]) = rq;
+            *reinterpret_cast<uint4*>(&sm.vb[r][swz(r, seg * 8)]) = rv;
         }
     }
     __syncthreads();
@@ -500,8 +523,8 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             bf16x8_t ak[2][NCT], aq[2][NCT], bh[2][NVT], bl[2][NVT];
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) {
-                ak[0][ct] = lds_frag_perm<32>(&kb[16 * ct + m][0], 0, gq);
-                aq[0][ct] = lds_frag_perm<32>(&sm.qb[16 * ct + m][0], 0, gq);
+                ak[0][ct] = row_frag(kb, 16 * ct + m, 0, gq);
+                aq[0][ct] = row_frag(sm.qb, 16 * ct + m, 0, gq);
             }
 #pragma unroll
             for (int vt = 0; vt < NVT; ++vt) acc_frag<32>(st[0][vt], st[1][vt], bh[0][vt], bl[0][vt]);
@@ -512,8 +535,8 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                 if (kq + 1 < D / 32) {
 #pragma unroll
                     for (int ct = 0; ct < NCT; ++ct) {
-                        ak[cur ^ 1][ct] = lds_frag_perm<32>(&kb[16 * ct + m][0], 32 * (kq + 1), gq);
-                        aq[cur ^ 1][ct] = lds_frag_perm<32>(&sm.qb[16 * ct + m][0], 32 * (kq + 1), gq);
+                        ak[cur ^ 1][ct] = row_frag(kb, 16 * ct + m, 32 * (kq + 1), gq);
+                        aq[cur ^ 1][ct] = row_frag(sm.qb, 16 * ct + m, 32 * (kq + 1), gq);
                     }
                 }
                 __builtin_amdgcn_sched_barrier(0);
@@ -558,7 +581,8 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
 #pragma unroll
                 for (int vt = 0; vt < NVT; ++vt) {
                     // V[16 ct + 4 gq + i][vcol0 + 16 vt + m], i = 0..3
-                    const uint2 vv = lds_tr4(&sm.vb[16 * ct + 4 * gq + (m >> 2)][vcol0 + 16 * vt + 4 * (m & 3)]);
+                    const int vr = 4 * gq + (m >> 2);
+                    const uint2 vv = lds_tr4(&sm.vb[16 * ct + vr][vcol0 + 16 * vt + swz(vr, 4 * (m & 3))]);
                     const float vf[4] = {bf16_to_f32(vv.x & 0xFFFFu), bf16_to_f32(vv.x >> 16),
                                          bf16_to_f32(vv.y & 0xFFFFu), bf16_to_f32(vv.y >> 16)};
 #pragma unroll
