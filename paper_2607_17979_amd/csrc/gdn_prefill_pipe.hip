@@ -229,6 +229,12 @@ __device__ __forceinline__ bf16x8_t row_frag(const uint16_t (*a)[PD], int r, int
     return __builtin_bit_cast(bf16x8_t, u);
 }
 
+// 16-byte global load at a wave-uniform base plus a 32-bit per-lane
+// byte offset (scalar base + vector offset addressing: no 64-bit lane math).
+__device__ __forceinline__ uint4 ld16(const void* base, unsigned byte_off) {
+    return *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(base) + byte_off);
+}
+
 // Producer work for chunk x (the j-th chunk of producer pc.pw).  The lane
 // indices m, gq are passed in per chunk (opaque to the compiler), so the
 // addresses and masks derived from them are recomputed per chunk instead of
@@ -259,7 +265,7 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
     auto load_frags = [&](const uint16_t* base, int b, uint4 (&f)[4]) {
         const unsigned off = (unsigned)min(16 * b + m, L - 1) * qks + 8u * gq;
 #pragma unroll
-        for (int kq = 0; kq < 4; ++kq) f[kq] = *reinterpret_cast<const uint4*>(base + off + 32 * kq);
+        for (int kq = 0; kq < 4; ++kq) f[kq] = ld16(base, 2u * off + 64u * kq);
     };
     uint4 fk[NCT][4], fq[2][4];
 #pragma unroll
@@ -409,8 +415,8 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
     for (int it = 0; it < SITEMS; ++it) {
         const unsigned off = (unsigned)min(4 * it + gq, L - 1) * qks + 8u * m;
         sk[it] = sq[it] = uint4{0, 0, 0, 0};
-        sk[it] = *reinterpret_cast<const uint4*>(kc0 + off);
-        sq[it] = *reinterpret_cast<const uint4*>(qc0 + off);
+        sk[it] = ld16(kc0, 2u * off);
+        sq[it] = ld16(qc0, 2u * off);
     }
     // K buffer x & 1 was last read by the update of chunk x - 2
     wait_ge(&sm.cnt[CNT_DONE], (unsigned)(x >= 2 ? NS * (x - 1) : 0));
@@ -424,7 +430,7 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
 #pragma unroll
     for (int it = 0; it < SITEMS; ++it) {
         sv[it] = uint4{0, 0, 0, 0};
-        sv[it] = *reinterpret_cast<const uint4*>(vc0 + (unsigned)min(4 * it + gq, L - 1) * (unsigned)pc.v_stride + 8u * m);
+        sv[it] = ld16(vc0, 2u * ((unsigned)min(4 * it + gq, L - 1) * (unsigned)pc.v_stride + 8u * m));
     }
 #pragma unroll
     for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.vb[4 * it + gq][swz(4 * it + gq, m * 8)]) = sv[it];
@@ -448,7 +454,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar chunk and address math
     const int m = lane & 15;
     const int gq = lane >> 4;
 
