@@ -458,7 +458,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
     const int m = lane & 15;
     const int gq = lane >> 4;
 
-    const int item = logical_item(blockIdx.x, N * H_v * VSPLIT);
+    const int item = logical_item<2 * VSPLIT>(blockIdx.x, N * H_v * VSPLIT);
     const int head_item = item / VSPLIT;
     const int vblock = item - head_item * VSPLIT;
     const int rank = head_item / H_v;
