@@ -28,6 +28,8 @@
 // bounded spin; LDS operations of a wave execute in order, so a counter
 // increment issued after a wave's LDS stores (or reads) is observed only after
 // those have executed.
+#include <algorithm>
+
 #include "gdn_launch.h"
 #include "gdn_mfma.h"
 
@@ -235,19 +237,20 @@ __device__ __forceinline__ uint4 ld16(const void* base, unsigned byte_off) {
     return *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(base) + byte_off);
 }
 
-// Producer work for chunk x (the j-th chunk of producer pc.pw).  The lane
-// indices m, gq are passed in per chunk (opaque to the compiler), so the
-// addresses and masks derived from them are recomputed per chunk instead of
-// being kept live across the producer loop.
+// Producer work for chunk lc of the work item described by pc, which is chunk
+// x of the workgroup's chunk stream (the chunks of its work items in order;
+// buffers and counters follow x).  The lane indices m, gq are passed in per
+// chunk (opaque to the compiler), so the addresses and masks derived from them
+// are recomputed per chunk instead of being kept live across the producer loop.
 template <int NS>
-__device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x, int j, int m, int gq) {
+__device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x, int lc, int m, int gq) {
     const int lane = m + 16 * gq;
     Slot& sl = sm.slot[pc.pw];
     float* scr = sm.scr[pc.pw];
     float* gam = sm.gam[pc.pw];
     float* bet = sm.bet[pc.pw];
-    const int L = min(C, pc.seq_len - x * C);
-    const int tb = pc.seq_beg + x * C;
+    const int L = min(C, pc.seq_len - lc * C);
+    const int tb = pc.seq_beg + lc * C;
     // ---- inputs: gates and the K operand fragments of the chunk
     //      (fk[b][kq]: row 16 b + m, columns 32 kq + 8 gq .. + 7); the Q
     //      fragments of block row b are loaded one block row ahead
@@ -406,7 +409,7 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
     signal(&sm.cnt[CNT_READY0 + pc.pw], lane);
     // ---- stage the chunk's K, Q, V rows once the state waves have
     //      released the previous chunk's (row 4 it + gq, segment m);
-    //      chunk 0 was staged by the whole workgroup
+    //      stream chunk 0 was staged by the whole workgroup
     if (x == 0) return;
     // (The zero stores before the loads are dead; without them the compiler
     // kept these arrays in scratch memory across the waits below.)
@@ -458,34 +461,58 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
     const int m = lane & 15;
     const int gq = lane >> 4;
 
-    const int item = logical_item<2 * VSPLIT>(blockIdx.x, N * H_v * VSPLIT);
-    const int head_item = item / VSPLIT;
-    const int vblock = item - head_item * VSPLIT;
-    const int rank = head_item / H_v;
-    const int h = head_item - rank * H_v;
-    const int n = order[rank];
-    const int hq = h / (H_v / H_qk);
-    const int seq_beg = cu[n];
-    const int seq_len = cu[n + 1] - seq_beg;
-    const int nch = (seq_len + C - 1) / C;
+    // Work items of this workgroup: on pass p the virtual index p G + b (b, or
+    // G - 1 - b on odd passes, which pairs long and short items) mapped to a
+    // logical item; -1 past the last item.
+    const int items = N * H_v * VSPLIT;
+    const int G = gridDim.x;
+    const int bid = blockIdx.x;
+    auto item_at = [&](int pass) -> int {
+        const int vb = pass * G + ((pass & 1) ? G - 1 - bid : bid);
+        return vb < items ? logical_item<2 * VSPLIT>(vb, items) : -1;
+    };
+    struct Item {
+        int n, h, hq, vblock, seq_beg, seq_len, nch;
+    };
+    auto decode = [&](int item) -> Item {
+        Item it;
+        const int head_item = item / VSPLIT;
+        it.vblock = item - head_item * VSPLIT;
+        const int rank = head_item / H_v;
+        it.h = head_item - rank * H_v;
+        it.n = order[rank];
+        it.hq = it.h / (H_v / H_qk);
+        it.seq_beg = cu[it.n];
+        it.seq_len = cu[it.n + 1] - it.seq_beg;
+        it.nch = (it.seq_len + C - 1) / C;
+        return it;
+    };
     const size_t qk_stride = (size_t)H_qk * D;
     const size_t v_stride = (size_t)H_v * D;
-    const size_t state_off = ((size_t)n * H_v + h) * D * D;
 
-    // Every wave stages chunk 0's K, Q, V rows before the roles split, so the
-    // state waves can start on it while producer 0 prepares the rest.
-    if (tid < NCNT) sm.cnt[tid] = (tid == CNT_STG && nch > 0) ? 1u : 0u;
+    // Every wave stages chunk 0 of the first non-empty item (chunk 0 of the
+    // stream) before the roles split, so the state waves can start on it while
+    // producer 0 prepares the rest.
+    Item first = {0, 0, 0, 0, 0, 0, 0};
+    for (int pass = 0;; ++pass) {
+        const int item = item_at(pass);
+        if (item < 0) break;
+        first = decode(item);
+        if (first.nch > 0) break;
+    }
+    if (tid < NCNT) sm.cnt[tid] = (tid == CNT_STG && first.nch > 0) ? 1u : 0u;
     for (int i = tid; i < 16 * 16; i += 64 * (NS + NP)) (&sm.zero[0][0])[i] = 0;
-    if (nch > 0) {
-        const int L0 = min(C, seq_len);
+    if (first.nch > 0) {
+        const int L0 = min(C, first.seq_len);
         for (int i = tid; i < C * SEGS; i += 64 * (NS + NP)) {
             const int r = i / SEGS, seg = i - r * SEGS;
             uint4 rk = {0, 0, 0, 0}, rq = {0, 0, 0, 0}, rv = {0, 0, 0, 0};
             if (r < L0) {
-                const size_t tq = (size_t)(seq_beg + r) * qk_stride + (size_t)hq * D + seg * 8;
+                const size_t tq = (size_t)(first.seq_beg + r) * qk_stride + (size_t)first.hq * D + seg * 8;
                 rk = *reinterpret_cast<const uint4*>(k + tq);
                 rq = *reinterpret_cast<const uint4*>(q + tq);
-                rv = *reinterpret_cast<const uint4*>(v + (size_t)(seq_beg + r) * v_stride + (size_t)h * D + seg * 8);
+                rv = *reinterpret_cast<const uint4*>(v + (size_t)(first.seq_beg + r) * v_stride + (size_t)first.h * D +
+                                                     seg * 8);
             }
             *reinterpret_cast<uint4*>(&sm.kb[0][r][swz(r, seg * 8)]) = rk;
             *reinterpret_cast<uint4*>(&sm.qb[r][swz(r, seg * 8)]) = rq;
@@ -496,8 +523,15 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
 
     if (wave < NS) {
         // ======================= state waves ===================================
-        const int vcol0 = (vblock * NS + wave) * VW;
         const SplitMasks spm = split_masks();
+        int xs = 0;  // stream index of the next chunk
+        for (int pass = 0;; ++pass) {
+        const int item = item_at(pass);
+        if (item < 0) break;
+        const Item it = decode(item);
+        const int h = it.h, seq_beg = it.seq_beg, seq_len = it.seq_len, nch = it.nch;
+        const size_t state_off = ((size_t)it.n * H_v + h) * D * D;
+        const int vcol0 = (it.vblock * NS + wave) * VW;
         f32x4_t st[NDT][NVT];  // st[dt][vt][i] = S[v][d], v = vcol0 + 16 vt + m, d = 16 dt + 4 gq + i
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt)
@@ -512,13 +546,13 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                 }
             }
 
-        for (int c = 0; c < nch; ++c) {
-            const int par = c & 1;
+        for (int c = 0; c < nch; ++c, ++xs) {
+            const int par = xs & 1;
             const int L = min(C, seq_len - c * C);
             const int t0 = seq_beg + c * C;
-            const Slot& sl = sm.slot[c % NP];
+            const Slot& sl = sm.slot[xs % NP];
             const uint16_t (*kb)[PD] = sm.kb[par];
-            wait_ge(&sm.cnt[CNT_STG], (unsigned)(c + 1));
+            wait_ge(&sm.cnt[CNT_STG], (unsigned)(xs + 1));
             // K S0^T (S0 hi + lo), rows t; (Q S0^T)^T (S0 hi), rows v
             f32x4_t ks[NCT][NVT], ot[NVT][NCT];
             const f32x4_t zero4 = {0.f, 0.f, 0.f, 0.f};
@@ -567,7 +601,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                 __builtin_amdgcn_sched_barrier(0);
             }
             // W = V - diag(exp(gamma)) K S0^T (in ks)
-            wait_ge(&sm.cnt[CNT_READY0 + c % NP], (unsigned)(c / NP + 1));
+            wait_ge(&sm.cnt[CNT_READY0 + xs % NP], (unsigned)(xs / NP + 1));
             // T operands of U = T diag(beta) W, read now so that their latency
             // hides behind the vector work of W
             bf16x8_t tah[NCT][2], tal[NCT][2];
@@ -726,13 +760,29 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                 *reinterpret_cast<float4*>(final_state + state_off + (size_t)(vcol0 + 16 * vt + m) * D +
                                            16 * dt + 4 * gq) = s4;
             }
+        }
     } else {
         // ======================= producer waves ================================
-        const ProdCtx pc = {q, k, v, g, beta, qk_stride, v_stride, seq_beg, seq_len, hq, h, H_v, wave - NS, scale};
-        for (int x = wave - NS, j = 0; x < nch; x += NP, ++j) {
+        ProdCtx pc = {q, k, v, g, beta, qk_stride, v_stride, 0, 0, 0, 0, H_v, wave - NS, scale};
+        // stream chunks x = pw, pw + NP, ...: the work item holding chunk x
+        // starts at stream index xbeg
+        int pass = 0, xbeg = 0;
+        int item = item_at(0);
+        Item it = item >= 0 ? decode(item) : first;
+        for (int x = wave - NS; item >= 0; x += NP) {
+            while (item >= 0 && x >= xbeg + it.nch) {
+                xbeg += it.nch;
+                item = item_at(++pass);
+                if (item >= 0) it = decode(item);
+            }
+            if (item < 0) break;
+            pc.seq_beg = it.seq_beg;
+            pc.seq_len = it.seq_len;
+            pc.hq = it.hq;
+            pc.h = it.h;
             int mo = m, go = gq;
             asm volatile("" : "+v"(mo), "+v"(go));
-            produce_chunk<NS>(sm, pc, x, j, mo, go);
+            produce_chunk<NS>(sm, pc, x, x - xbeg, mo, go);
         }
     }
 }
@@ -751,10 +801,14 @@ static int compute_units() {
     return n;
 }
 
+// One workgroup per compute unit (the LDS use admits one), each walking its
+// work items; fewer items than compute units give one item per workgroup.
 template <int NS, int NVT>
 static hipError_t launch_pipe(const PrefillArgs& a, const int32_t* order, hipStream_t stream) {
     constexpr int VSPLIT = pipe::D / (16 * NS * NVT);
-    hipLaunchKernelGGL((pipe::prefill_pipe_kernel<NS, NVT>), dim3((unsigned)(a.N * a.H_v * VSPLIT)),
+    const long items = (long)a.N * a.H_v * VSPLIT;
+    const long grid = std::min<long>(items, compute_units());
+    hipLaunchKernelGGL((pipe::prefill_pipe_kernel<NS, NVT>), dim3((unsigned)grid),
                        dim3(64 * (NS + pipe::NP)), 0, stream, (const uint16_t*)a.q, (const uint16_t*)a.k,
                        (const uint16_t*)a.v, a.g, a.beta, a.cu_seqlens, order, a.initial_state, a.final_state,
                        (uint16_t*)a.o, a.N, a.H_qk, a.H_v, a.scale);

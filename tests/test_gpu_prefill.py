@@ -213,3 +213,38 @@ def test_prefill_value_split_is_bitwise_batch_independent():
         for c in range(copies):
             assert torch.equal(o[c * L:(c + 1) * L].view(torch.int16), o1.view(torch.int16)), (copies, c)
             assert torch.equal(f[c].view(torch.int32), f1[0].view(torch.int32)), (copies, c)
+
+
+def test_prefill_several_items_per_workgroup():
+    """48 sequences x 32 value heads = 1,536 work items, more than the
+    workgroups launched (one per compute unit), so each workgroup walks several
+    items as one chunk stream: lengths from 0 to 260 (zero-length ones, single
+    tokens, chunk boundaries 63/64/65) from a nonzero initial state.  The
+    oracle follows two heads of every sequence; zero-length sequences keep
+    their initial state bit for bit; three sequences run alone give bitwise
+    the same outputs and states as inside the large batch."""
+    import torch
+
+    dev = device()
+    rng = np.random.default_rng(77)
+    lengths = rng.integers(0, 261, size=48)
+    lengths[[3, 17, 30, 41]] = 0
+    lengths[[5, 6, 7, 8]] = [1, 63, 64, 65]
+    H_qk, H_v, D = 16, 32, 128
+    note(f"prefill several items per workgroup: N=48, T={lengths.sum()}")
+    inp = wl.prefill_inputs(78, lengths, H_qk, H_v, D, state_std=0.02, scale=D ** -0.5)
+    o, fin = _prefill_gpu(inp, dev)
+    units = [(n, h) for n in range(48) for h in ((7 * n) % H_v, (7 * n + 13) % H_v)]
+    _sampled_check(inp, o, fin, units, "several items per workgroup")
+    fin_np = fin.cpu().numpy()
+    for n in np.nonzero(lengths == 0)[0]:
+        assert np.array_equal(fin_np[n], inp.initial_state[n]), n
+    cu = inp.cu_seqlens
+    for n in (0, 7, int(np.argmax(lengths))):
+        a, b = cu[n], cu[n + 1]
+        one = wl.PrefillInputs(q=inp.q[a:b], k=inp.k[a:b], v=inp.v[a:b], g=inp.g[a:b], beta=inp.beta[a:b],
+                               cu_seqlens=np.array([0, b - a], dtype=np.int32),
+                               initial_state=inp.initial_state[n:n + 1], scale=inp.scale)
+        o1, f1 = _prefill_gpu(one, dev)
+        assert torch.equal(o[a:b].view(torch.int16), o1.view(torch.int16)), n
+        assert torch.equal(fin[n].view(torch.int32), f1[0].view(torch.int32)), n
