@@ -69,21 +69,31 @@ struct Slot {
 
 enum {
     CNT_STG = 0,      // chunks whose K, Q and V rows are staged
-    CNT_QVFREE,       // state-wave releases of the Q and V row buffers (after W)
-    CNT_DONE,         // state-wave chunk completions: the chunk's K buffer and slot are free
+    CNT_QVFREE,       // releases of the Q and V row buffers (state waves after W,
+                      // output waves after (Q S0^T)^T)
+    CNT_DONE,         // chunk completions (state and output waves): the chunk's
+                      // K buffer and result slot are free
     CNT_READY0,       // + p: chunks written to slot p
-    NCNT = CNT_READY0 + NP
+    CNT_HAND0 = CNT_READY0 + NP,  // + 4 w + {0, 1, 2, 3}: S0 hi operands of state
+                      // wave w written / read, U hi operands written / read
+    NCNT = CNT_HAND0 + 4 * 2
 };
 
+// VB: value columns of the workgroup (the V rows it stages); NO: output waves,
+// each finishing (Q S0^T)^T, the output products and the stores for one state
+// wave, fed through the hand-over arrays.
+template <int VB, int NO, int NVT>
 struct Smem {
     uint16_t kb[2][C][PD];            // K rows, by chunk parity
-    uint16_t qb[C][PD];               // Q rows of the chunk the state waves work on
-    uint16_t vb[C][PD];               // V rows
+    uint16_t qb[C][PD];               // Q rows of the chunk in flight
+    uint16_t vb[C][VB + 16];          // V rows, the workgroup's columns (swizzled, see PD)
     Slot slot[NP];
     alignas(16) float scr[NP][NCT * 16 * SP];  // per producer: diagonal blocks of A, then of T
     alignas(16) float gam[NP][C];     // per producer: gate prefix of its chunk
     alignas(16) float bet[NP][C];     // per producer: beta of its chunk
     uint16_t zero[16][16];            // stands in for blocks above the diagonal
+    uint4 hs[NO][D / 32][NVT][64];    // per state wave: S0 hi operands of the chunk
+    uint4 hu[NO][C / 32][NVT][64];    // per state wave: U hi operands of the chunk
     unsigned cnt[NCNT];
 };
 
@@ -217,6 +227,7 @@ struct ProdCtx {
     const float* beta;
     size_t qk_stride, v_stride;
     int seq_beg, seq_len, hq, h, H_v, pw;
+    int vcb0;   // first value column of the workgroup
     float scale;
 };
 
@@ -242,8 +253,10 @@ __device__ __forceinline__ uint4 ld16(const void* base, unsigned byte_off) {
 // buffers and counters follow x).  The lane indices m, gq are passed in per
 // chunk (opaque to the compiler), so the addresses and masks derived from them
 // are recomputed per chunk instead of being kept live across the producer loop.
-template <int NS>
-__device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x, int lc, int m, int gq) {
+// NSIG: waves that count each chunk done and each Q/V release (state plus
+// output waves); VB: value columns staged.
+template <int NSIG, int VB, class SM>
+__device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, int lc, int m, int gq) {
     const int lane = m + 16 * gq;
     Slot& sl = sm.slot[pc.pw];
     float* scr = sm.scr[pc.pw];
@@ -392,7 +405,7 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
     }
     // ---- publish to the slot once the state waves are done with its
     //      previous chunk
-    wait_ge(&sm.cnt[CNT_DONE], (unsigned)(x >= 4 ? NS * (x - 3) : 0));   // chunk x - 4 done
+    wait_ge(&sm.cnt[CNT_DONE], (unsigned)(x >= 4 ? NSIG * (x - 3) : 0));   // chunk x - 4 done
 #pragma unroll
     for (int b = 0; b < NCT; ++b)
 #pragma unroll
@@ -422,21 +435,25 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
         sq[it] = ld16(qc0, 2u * off);
     }
     // K buffer x & 1 was last read by the update of chunk x - 2
-    wait_ge(&sm.cnt[CNT_DONE], (unsigned)(x >= 2 ? NS * (x - 1) : 0));
+    wait_ge(&sm.cnt[CNT_DONE], (unsigned)(x >= 2 ? NSIG * (x - 1) : 0));
 #pragma unroll
     for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.kb[x & 1][4 * it + gq][swz(4 * it + gq, m * 8)]) = sk[it];
-    wait_ge(&sm.cnt[CNT_QVFREE], (unsigned)(NS * x));
+    wait_ge(&sm.cnt[CNT_QVFREE], (unsigned)(NSIG * x));
 #pragma unroll
     for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.qb[4 * it + gq][swz(4 * it + gq, m * 8)]) = sq[it];
-    const uint16_t* vc0 = pc.v + (size_t)tb * pc.v_stride + (size_t)pc.h * D;
-    uint4 sv[SITEMS];
+    // V rows of the workgroup's VB columns: VB / 8 lanes per row
+    constexpr int VLR = VB / 8, VRI = 64 / VLR, VIT = C / VRI;
+    const int vr = lane / VLR, vsg = lane - vr * VLR;
+    const uint16_t* vc0 = pc.v + (size_t)tb * pc.v_stride + (size_t)pc.h * D + pc.vcb0;
+    uint4 sv[VIT];
 #pragma unroll
-    for (int it = 0; it < SITEMS; ++it) {
+    for (int it = 0; it < VIT; ++it) {
         sv[it] = uint4{0, 0, 0, 0};
-        sv[it] = ld16(vc0, 2u * ((unsigned)min(4 * it + gq, L - 1) * (unsigned)pc.v_stride + 8u * m));
+        sv[it] = ld16(vc0, 2u * ((unsigned)min(VRI * it + vr, L - 1) * (unsigned)pc.v_stride + 8u * vsg));
     }
 #pragma unroll
-    for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.vb[4 * it + gq][swz(4 * it + gq, m * 8)]) = sv[it];
+    for (int it = 0; it < VIT; ++it)
+        *reinterpret_cast<uint4*>(&sm.vb[VRI * it + vr][swz(VRI * it + vr, 8 * vsg)]) = sv[it];
     signal(&sm.cnt[CNT_STG], lane);
 }
 
@@ -444,16 +461,19 @@ __device__ __forceinline__ void produce_chunk(Smem& sm, const ProdCtx& pc, int x
 // covers NS * NVT * 16 of the D value columns of its head, so a head is split
 // over VSPLIT = D / (16 NS NVT) workgroups (each repeating the producer work of
 // the head), which spreads few long sequences over more compute units.
-template <int NS, int NVT>
-__global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
+template <int NS, int NVT, int NO>
+__global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const float* __restrict__ g, const float* __restrict__ beta, const int32_t* __restrict__ cu,
     const int32_t* __restrict__ order, const float* initial_state, float* final_state,
     uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale) {
     constexpr int VW = 16 * NVT;        // value columns per state wave
-    constexpr int VSPLIT = D / (NS * VW);
-    static_assert(VSPLIT * NS * VW == D, "value columns must tile D");
-    __shared__ Smem sm;
+    constexpr int VB = NS * VW;         // value columns per workgroup
+    constexpr int VSPLIT = D / VB;
+    constexpr int NW = NS + NO + NP;    // waves per workgroup
+    static_assert(VSPLIT * VB == D, "value columns must tile D");
+    static_assert(NO == 0 || NO == NS, "one output wave per state wave");
+    __shared__ Smem<VB, NO, NVT> sm;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -501,21 +521,26 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
         if (first.nch > 0) break;
     }
     if (tid < NCNT) sm.cnt[tid] = (tid == CNT_STG && first.nch > 0) ? 1u : 0u;
-    for (int i = tid; i < 16 * 16; i += 64 * (NS + NP)) (&sm.zero[0][0])[i] = 0;
+    for (int i = tid; i < 16 * 16; i += 64 * NW) (&sm.zero[0][0])[i] = 0;
     if (first.nch > 0) {
         const int L0 = min(C, first.seq_len);
-        for (int i = tid; i < C * SEGS; i += 64 * (NS + NP)) {
+        for (int i = tid; i < C * SEGS; i += 64 * NW) {
             const int r = i / SEGS, seg = i - r * SEGS;
-            uint4 rk = {0, 0, 0, 0}, rq = {0, 0, 0, 0}, rv = {0, 0, 0, 0};
+            uint4 rk = {0, 0, 0, 0}, rq = {0, 0, 0, 0};
             if (r < L0) {
                 const size_t tq = (size_t)(first.seq_beg + r) * qk_stride + (size_t)first.hq * D + seg * 8;
                 rk = *reinterpret_cast<const uint4*>(k + tq);
                 rq = *reinterpret_cast<const uint4*>(q + tq);
-                rv = *reinterpret_cast<const uint4*>(v + (size_t)(first.seq_beg + r) * v_stride + (size_t)first.h * D +
-                                                     seg * 8);
             }
             *reinterpret_cast<uint4*>(&sm.kb[0][r][swz(r, seg * 8)]) = rk;
             *reinterpret_cast<uint4*>(&sm.qb[r][swz(r, seg * 8)]) = rq;
+        }
+        for (int i = tid; i < C * (VB / 8); i += 64 * NW) {
+            const int r = i / (VB / 8), seg = i - r * (VB / 8);
+            uint4 rv = {0, 0, 0, 0};
+            if (r < L0)
+                rv = *reinterpret_cast<const uint4*>(v + (size_t)(first.seq_beg + r) * v_stride + (size_t)first.h * D +
+                                                     first.vblock * VB + seg * 8);
             *reinterpret_cast<uint4*>(&sm.vb[r][swz(r, seg * 8)]) = rv;
         }
     }
@@ -553,7 +578,10 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             const Slot& sl = sm.slot[xs % NP];
             const uint16_t (*kb)[PD] = sm.kb[par];
             wait_ge(&sm.cnt[CNT_STG], (unsigned)(xs + 1));
-            // K S0^T (S0 hi + lo), rows t; (Q S0^T)^T (S0 hi), rows v
+            // with output waves: the previous chunk's S0 hi operands were read
+            if constexpr (NO > 0) wait_ge(&sm.cnt[CNT_HAND0 + 4 * wave + 1], (unsigned)xs);
+            // K S0^T (S0 hi + lo), rows t; (Q S0^T)^T (S0 hi), rows v, unless
+            // an output wave takes it (it gets the S0 hi operands instead)
             f32x4_t ks[NCT][NVT], ot[NVT][NCT];
             const f32x4_t zero4 = {0.f, 0.f, 0.f, 0.f};
             // Software pipeline over the contraction: the operand reads of step
@@ -564,10 +592,13 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) {
                 ak[0][ct] = row_frag(kb, 16 * ct + m, 0, gq);
-                aq[0][ct] = row_frag(sm.qb, 16 * ct + m, 0, gq);
+                if constexpr (NO == 0) aq[0][ct] = row_frag(sm.qb, 16 * ct + m, 0, gq);
             }
 #pragma unroll
-            for (int vt = 0; vt < NVT; ++vt) acc_frag<32>(st[0][vt], st[1][vt], bh[0][vt], bl[0][vt]);
+            for (int vt = 0; vt < NVT; ++vt) {
+                acc_frag<32>(st[0][vt], st[1][vt], bh[0][vt], bl[0][vt]);
+                if constexpr (NO > 0) sm.hs[wave % (NO > 0 ? NO : 1)][0][vt][lane] = __builtin_bit_cast(uint4, bh[0][vt]);
+            }
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int kq = 0; kq < D / 32; ++kq) {
@@ -576,14 +607,17 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
 #pragma unroll
                     for (int ct = 0; ct < NCT; ++ct) {
                         ak[cur ^ 1][ct] = row_frag(kb, 16 * ct + m, 32 * (kq + 1), gq);
-                        aq[cur ^ 1][ct] = row_frag(sm.qb, 16 * ct + m, 32 * (kq + 1), gq);
+                        if constexpr (NO == 0) aq[cur ^ 1][ct] = row_frag(sm.qb, 16 * ct + m, 32 * (kq + 1), gq);
                     }
                 }
                 __builtin_amdgcn_sched_barrier(0);
                 if (kq + 1 < D / 32) {
 #pragma unroll
-                    for (int vt = 0; vt < NVT; ++vt)
+                    for (int vt = 0; vt < NVT; ++vt) {
                         acc_frag<32>(st[2 * kq + 2][vt], st[2 * kq + 3][vt], bh[cur ^ 1][vt], bl[cur ^ 1][vt]);
+                        if constexpr (NO > 0)
+                            sm.hs[wave % (NO > 0 ? NO : 1)][kq + 1][vt][lane] = __builtin_bit_cast(uint4, bh[cur ^ 1][vt]);
+                    }
                 }
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct)
@@ -591,7 +625,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     for (int vt = 0; vt < NVT; ++vt) {
                         ks[ct][vt] = mma(ak[cur][ct], bh[cur][vt], kq == 0 ? zero4 : ks[ct][vt]);
                         ks[ct][vt] = mma(ak[cur][ct], bl[cur][vt], ks[ct][vt]);
-                        ot[vt][ct] = mma(bh[cur][vt], aq[cur][ct], kq == 0 ? zero4 : ot[vt][ct]);
+                        if constexpr (NO == 0) ot[vt][ct] = mma(bh[cur][vt], aq[cur][ct], kq == 0 ? zero4 : ot[vt][ct]);
                     }
 #pragma unroll
                 for (int i = 0; i < 4 * NVT; ++i) {
@@ -600,6 +634,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
+            if constexpr (NO > 0) signal(&sm.cnt[CNT_HAND0 + 4 * wave + 0], lane);
             // W = V - diag(exp(gamma)) K S0^T (in ks)
             wait_ge(&sm.cnt[CNT_READY0 + xs % NP], (unsigned)(xs / NP + 1));
             // T operands of U = T diag(beta) W, read now so that their latency
@@ -622,7 +657,7 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                 for (int vt = 0; vt < NVT; ++vt) {
                     // V[16 ct + 4 gq + i][vcol0 + 16 vt + m], i = 0..3
                     const int vr = 4 * gq + (m >> 2);
-                    const uint2 vv = lds_tr4(&sm.vb[16 * ct + vr][vcol0 + 16 * vt + swz(vr, 4 * (m & 3))]);
+                    const uint2 vv = lds_tr4(&sm.vb[16 * ct + vr][wave * VW + 16 * vt + swz(vr, 4 * (m & 3))]);
                     const float vf[4] = {bf16_to_f32(vv.x & 0xFFFFu), bf16_to_f32(vv.x >> 16),
                                          bf16_to_f32(vv.y & 0xFFFFu), bf16_to_f32(vv.y >> 16)};
 #pragma unroll
@@ -664,6 +699,17 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     }
                 }
             }
+            if constexpr (NO > 0) {
+                // the previous chunk's U hi operands were read
+                wait_ge(&sm.cnt[CNT_HAND0 + 4 * wave + 3], (unsigned)xs);
+#pragma unroll
+                for (int kc = 0; kc < C; kc += 32)
+#pragma unroll
+                    for (int vt = 0; vt < NVT; ++vt)
+                        sm.hu[wave % (NO > 0 ? NO : 1)][kc / 32][vt][lane] =
+                            __builtin_bit_cast(uint4, acc_frag_hi<32>(uu[kc / 16][vt], uu[kc / 16 + 1][vt]));
+                signal(&sm.cnt[CNT_HAND0 + 4 * wave + 2], lane);
+            }
             // S^T = exp(gamma_last) S^T + K^T (diag(exp(gamma_last - gamma)) U)   (hi + lo),
             // block row by block row of S^T so that the scaling of one overlaps
             // the products of the previous
@@ -673,13 +719,15 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             const float eg_last = sl.eg[C - 1];
             // P operands of the output products, read ahead of the update
             bf16x8_t pf[NCT][2];
+            if constexpr (NO == 0) {
 #pragma unroll
-            for (int ct = 0; ct < NCT; ++ct)
+                for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-                for (int hb = 0; hb < 2; ++hb) {
-                    if (32 * hb > 16 * ct + 15) continue;
-                    pf[ct][hb] = blk_frag(sl.pm, sm.zero, ct, 32 * hb, m, gq);
-                }
+                    for (int hb = 0; hb < 2; ++hb) {
+                        if (32 * hb > 16 * ct + 15) continue;
+                        pf[ct][hb] = blk_frag(sl.pm, sm.zero, ct, 32 * hb, m, gq);
+                    }
+            }
             bf16x8_t uth[2][NVT], utl[2][NVT];
 #pragma unroll
             for (int hb = 0; hb < 2; ++hb)
@@ -700,56 +748,60 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                     st[dt][vt] = mma(a1, utl[1][vt], st[dt][vt]);
                 }
             }
-            // scale O^T = scale diag(exp(gamma)) (Q S0^T)^T + U^T (scale M o Q K^T)^T
-            // (U hi); its vector work overlaps the update's products
-#pragma unroll
-            for (int ct = 0; ct < NCT; ++ct) {
-                const float e = sl.eg[16 * ct + m] * scale;
-#pragma unroll
-                for (int vt = 0; vt < NVT; ++vt) ot[vt][ct] *= e;
-            }
-#pragma unroll
-            for (int kc = 0; kc < C; kc += 32) {
-                bf16x8_t uh[NVT];
-#pragma unroll
-                for (int vt = 0; vt < NVT; ++vt) uh[vt] = acc_frag_hi<32>(uu[kc / 16][vt], uu[kc / 16 + 1][vt]);
+            if constexpr (NO == 0) {
+                // scale O^T = scale diag(exp(gamma)) (Q S0^T)^T + U^T (scale M o Q K^T)^T
+                // (U hi); its vector work overlaps the update's products
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) {
-                    if (kc > 16 * ct + 15) continue;
-                    const bf16x8_t& bp = pf[ct][kc / 32];
+                    const float e = sl.eg[16 * ct + m] * scale;
 #pragma unroll
-                    for (int vt = 0; vt < NVT; ++vt) ot[vt][ct] = mma(uh[vt], bp, ot[vt][ct]);
+                    for (int vt = 0; vt < NVT; ++vt) ot[vt][ct] *= e;
+                }
+#pragma unroll
+                for (int kc = 0; kc < C; kc += 32) {
+                    bf16x8_t uh[NVT];
+#pragma unroll
+                    for (int vt = 0; vt < NVT; ++vt) uh[vt] = acc_frag_hi<32>(uu[kc / 16][vt], uu[kc / 16 + 1][vt]);
+#pragma unroll
+                    for (int ct = 0; ct < NCT; ++ct) {
+                        if (kc > 16 * ct + 15) continue;
+                        const bf16x8_t& bp = pf[ct][kc / 32];
+#pragma unroll
+                        for (int vt = 0; vt < NVT; ++vt) ot[vt][ct] = mma(uh[vt], bp, ot[vt][ct]);
+                    }
                 }
             }
             // all LDS reads of chunk c are done: its K buffer and result slot are free
             signal(&sm.cnt[CNT_DONE], lane);
-            // Outputs: lane m + 16 gq holds, in ot[vt][ct], token 16 ct + m and
-            // value columns 16 vt + 4 gq .. + 3.  Two such tiles x, y are merged
-            // by a swap between lane groups gq and gq ^ 1 (v_permlane16_swap:
-            // group 2i ends with x of groups 2i, 2i + 1, group 2i + 1 with y of
-            // both), so that each lane stores 8 consecutive columns (16 bytes):
-            // x, y are the two value tiles when NVT is even, else token blocks
-            // ct and ct + 1.
-            const int odd = gq & 1, half = gq >> 1;
-            auto store_pair = [&](const f32x4_t& x, const f32x4_t& y, int row, int col) {
-                const auto p0 = __builtin_amdgcn_permlane16_swap(cvt_pk(x[0], x[1]), cvt_pk(y[0], y[1]), false, false);
-                const auto p1 = __builtin_amdgcn_permlane16_swap(cvt_pk(x[2], x[3]), cvt_pk(y[2], y[3]), false, false);
-                const uint4 pk = {p0[0], p1[0], p0[1], p1[1]};
-                if (row < L)
-                    *reinterpret_cast<uint4*>(o + (size_t)(t0 + row) * v_stride + (size_t)h * D + vcol0 + col) = pk;
-            };
-            if constexpr (NVT % 2 == 0) {
+            if constexpr (NO == 0) {
+                // Outputs: lane m + 16 gq holds, in ot[vt][ct], token 16 ct + m and
+                // value columns 16 vt + 4 gq .. + 3.  Two such tiles x, y are merged
+                // by a swap between lane groups gq and gq ^ 1 (v_permlane16_swap:
+                // group 2i ends with x of groups 2i, 2i + 1, group 2i + 1 with y of
+                // both), so that each lane stores 8 consecutive columns (16 bytes):
+                // x, y are the two value tiles when NVT is even, else token blocks
+                // ct and ct + 1.
+                const int odd = gq & 1, half = gq >> 1;
+                auto store_pair = [&](const f32x4_t& x, const f32x4_t& y, int row, int col) {
+                    const auto p0 = __builtin_amdgcn_permlane16_swap(cvt_pk(x[0], x[1]), cvt_pk(y[0], y[1]), false, false);
+                    const auto p1 = __builtin_amdgcn_permlane16_swap(cvt_pk(x[2], x[3]), cvt_pk(y[2], y[3]), false, false);
+                    const uint4 pk = {p0[0], p1[0], p0[1], p1[1]};
+                    if (row < L)
+                        *reinterpret_cast<uint4*>(o + (size_t)(t0 + row) * v_stride + (size_t)h * D + vcol0 + col) = pk;
+                };
+                if constexpr (NVT % 2 == 0) {
 #pragma unroll
-                for (int ct = 0; ct < NCT; ++ct)
+                    for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-                    for (int vt = 0; vt < NVT; vt += 2)
-                        store_pair(ot[vt][ct], ot[vt + 1][ct], 16 * ct + m, 16 * vt + 16 * odd + 8 * half);
-            } else {
+                        for (int vt = 0; vt < NVT; vt += 2)
+                            store_pair(ot[vt][ct], ot[vt + 1][ct], 16 * ct + m, 16 * vt + 16 * odd + 8 * half);
+                } else {
 #pragma unroll
-                for (int ct = 0; ct < NCT; ct += 2)
+                    for (int ct = 0; ct < NCT; ct += 2)
 #pragma unroll
-                    for (int vt = 0; vt < NVT; ++vt)
-                        store_pair(ot[vt][ct], ot[vt][ct + 1], 16 * (ct + odd) + m, 16 * vt + 8 * half);
+                        for (int vt = 0; vt < NVT; ++vt)
+                            store_pair(ot[vt][ct], ot[vt][ct + 1], 16 * (ct + odd) + m, 16 * vt + 8 * half);
+                }
             }
         }
 #pragma unroll
@@ -761,15 +813,112 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
                                            16 * dt + 4 * gq) = s4;
             }
         }
+    } else if (wave < NS + NO) {
+        // ======================= output waves ==================================
+        // Output wave w finishes the chunks of state wave w: (Q S0^T)^T from
+        // the handed-over S0 hi operands, then the output products with the
+        // handed-over U hi operands, then the stores.
+        const int w = wave - NS;
+        int xs = 0;
+        for (int pass = 0;; ++pass) {
+            const int item = item_at(pass);
+            if (item < 0) break;
+            const Item it = decode(item);
+            const int vcol0 = (it.vblock * NS + w) * VW;
+            for (int c = 0; c < it.nch; ++c, ++xs) {
+                const int L = min(C, it.seq_len - c * C);
+                const int t0 = it.seq_beg + c * C;
+                const Slot& sl = sm.slot[xs % NP];
+                const f32x4_t zero4 = {0.f, 0.f, 0.f, 0.f};
+                // the chunk's Q operands go to registers at once, so that the Q
+                // buffer is released before the S0 operands arrive
+                wait_ge(&sm.cnt[CNT_STG], (unsigned)(xs + 1));
+                bf16x8_t aq[D / 32][NCT];
+#pragma unroll
+                for (int kq = 0; kq < D / 32; ++kq)
+#pragma unroll
+                    for (int ct = 0; ct < NCT; ++ct) aq[kq][ct] = row_frag(sm.qb, 16 * ct + m, 32 * kq, gq);
+                signal(&sm.cnt[CNT_QVFREE], lane);
+                wait_ge(&sm.cnt[CNT_HAND0 + 4 * w + 0], (unsigned)(xs + 1));
+                bf16x8_t bh[D / 32][NVT];
+#pragma unroll
+                for (int kq = 0; kq < D / 32; ++kq)
+#pragma unroll
+                    for (int vt = 0; vt < NVT; ++vt) bh[kq][vt] = __builtin_bit_cast(bf16x8_t, sm.hs[w % (NO > 0 ? NO : 1)][kq][vt][lane]);
+                signal(&sm.cnt[CNT_HAND0 + 4 * w + 1], lane);
+                f32x4_t ot[NVT][NCT];
+#pragma unroll
+                for (int kq = 0; kq < D / 32; ++kq)
+#pragma unroll
+                    for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                        for (int vt = 0; vt < NVT; ++vt) ot[vt][ct] = mma(bh[kq][vt], aq[kq][ct], kq == 0 ? zero4 : ot[vt][ct]);
+                wait_ge(&sm.cnt[CNT_READY0 + xs % NP], (unsigned)(xs / NP + 1));
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) {
+                    const float e = sl.eg[16 * ct + m] * scale;
+#pragma unroll
+                    for (int vt = 0; vt < NVT; ++vt) ot[vt][ct] *= e;
+                }
+                bf16x8_t pf[NCT][2];
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                    for (int hb = 0; hb < 2; ++hb) {
+                        if (32 * hb > 16 * ct + 15) continue;
+                        pf[ct][hb] = blk_frag(sl.pm, sm.zero, ct, 32 * hb, m, gq);
+                    }
+                wait_ge(&sm.cnt[CNT_HAND0 + 4 * w + 2], (unsigned)(xs + 1));
+                bf16x8_t uh[C / 32][NVT];
+#pragma unroll
+                for (int kc = 0; kc < C / 32; ++kc)
+#pragma unroll
+                    for (int vt = 0; vt < NVT; ++vt) uh[kc][vt] = __builtin_bit_cast(bf16x8_t, sm.hu[w % (NO > 0 ? NO : 1)][kc][vt][lane]);
+                signal(&sm.cnt[CNT_HAND0 + 4 * w + 3], lane);
+#pragma unroll
+                for (int kc = 0; kc < C; kc += 32)
+#pragma unroll
+                    for (int ct = 0; ct < NCT; ++ct) {
+                        if (kc > 16 * ct + 15) continue;
+#pragma unroll
+                        for (int vt = 0; vt < NVT; ++vt) ot[vt][ct] = mma(uh[kc / 32][vt], pf[ct][kc / 32], ot[vt][ct]);
+                    }
+                // all LDS reads of the chunk by this wave are done
+                signal(&sm.cnt[CNT_DONE], lane);
+                // outputs: token blocks ct and ct + 1 (or the value tiles) merged by
+                // a swap between lane groups, 8 consecutive columns per lane
+                const int odd = gq & 1, half = gq >> 1;
+                auto store_pair = [&](const f32x4_t& x, const f32x4_t& y, int row, int col) {
+                    const auto p0 = __builtin_amdgcn_permlane16_swap(cvt_pk(x[0], x[1]), cvt_pk(y[0], y[1]), false, false);
+                    const auto p1 = __builtin_amdgcn_permlane16_swap(cvt_pk(x[2], x[3]), cvt_pk(y[2], y[3]), false, false);
+                    const uint4 pk = {p0[0], p1[0], p0[1], p1[1]};
+                    if (row < L)
+                        *reinterpret_cast<uint4*>(o + (size_t)(t0 + row) * v_stride + (size_t)it.h * D + vcol0 + col) = pk;
+                };
+                if constexpr (NVT % 2 == 0) {
+#pragma unroll
+                    for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                        for (int vt = 0; vt < NVT; vt += 2)
+                            store_pair(ot[vt][ct], ot[vt + 1][ct], 16 * ct + m, 16 * vt + 16 * odd + 8 * half);
+                } else {
+#pragma unroll
+                    for (int ct = 0; ct < NCT; ct += 2)
+#pragma unroll
+                        for (int vt = 0; vt < NVT; ++vt)
+                            store_pair(ot[vt][ct], ot[vt][ct + 1], 16 * (ct + odd) + m, 16 * vt + 8 * half);
+                }
+            }
+        }
     } else {
         // ======================= producer waves ================================
-        ProdCtx pc = {q, k, v, g, beta, qk_stride, v_stride, 0, 0, 0, 0, H_v, wave - NS, scale};
+        ProdCtx pc = {q, k, v, g, beta, qk_stride, v_stride, 0, 0, 0, 0, H_v, wave - NS - NO, 0, scale};
         // stream chunks x = pw, pw + NP, ...: the work item holding chunk x
         // starts at stream index xbeg
         int pass = 0, xbeg = 0;
         int item = item_at(0);
         Item it = item >= 0 ? decode(item) : first;
-        for (int x = wave - NS; item >= 0; x += NP) {
+        for (int x = wave - NS - NO; item >= 0; x += NP) {
             while (item >= 0 && x >= xbeg + it.nch) {
                 xbeg += it.nch;
                 item = item_at(++pass);
@@ -780,9 +929,10 @@ __global__ __launch_bounds__(64 * (NS + NP)) void prefill_pipe_kernel(
             pc.seq_len = it.seq_len;
             pc.hq = it.hq;
             pc.h = it.h;
+            pc.vcb0 = it.vblock * VB;
             int mo = m, go = gq;
             asm volatile("" : "+v"(mo), "+v"(go));
-            produce_chunk<NS>(sm, pc, x, x - xbeg, mo, go);
+            produce_chunk<NS + NO, VB>(sm, pc, x, x - xbeg, mo, go);
         }
     }
 }
@@ -803,13 +953,13 @@ static int compute_units() {
 
 // One workgroup per compute unit (the LDS use admits one), each walking its
 // work items; fewer items than compute units give one item per workgroup.
-template <int NS, int NVT>
+template <int NS, int NVT, int NO>
 static hipError_t launch_pipe(const PrefillArgs& a, const int32_t* order, hipStream_t stream) {
     constexpr int VSPLIT = pipe::D / (16 * NS * NVT);
     const long items = (long)a.N * a.H_v * VSPLIT;
     const long grid = std::min<long>(items, compute_units());
-    hipLaunchKernelGGL((pipe::prefill_pipe_kernel<NS, NVT>), dim3((unsigned)grid),
-                       dim3(64 * (NS + pipe::NP)), 0, stream, (const uint16_t*)a.q, (const uint16_t*)a.k,
+    hipLaunchKernelGGL((pipe::prefill_pipe_kernel<NS, NVT, NO>), dim3((unsigned)grid),
+                       dim3(64 * (NS + NO + pipe::NP)), 0, stream, (const uint16_t*)a.q, (const uint16_t*)a.k,
                        (const uint16_t*)a.v, a.g, a.beta, a.cu_seqlens, order, a.initial_state, a.final_state,
                        (uint16_t*)a.o, a.N, a.H_qk, a.H_v, a.scale);
     return hipGetLastError();
@@ -821,9 +971,9 @@ static hipError_t launch_pipe(const PrefillArgs& a, const int32_t* order, hipStr
 hipError_t launch_prefill_pipe(const PrefillArgs& a, const int32_t* order, hipStream_t stream) {
     const long heads = (long)a.N * a.H_v;
     const long cus = compute_units();
-    if (heads * 4 <= cus) return launch_pipe<2, 1>(a, order, stream);
-    if (heads * 2 <= cus) return launch_pipe<4, 1>(a, order, stream);
-    return launch_pipe<4, 2>(a, order, stream);
+    if (heads * 4 <= cus) return launch_pipe<2, 1, 2>(a, order, stream);
+    if (heads * 2 <= cus) return launch_pipe<4, 1, 0>(a, order, stream);
+    return launch_pipe<4, 2, 0>(a, order, stream);
 }
 
 }  // namespace gdn
