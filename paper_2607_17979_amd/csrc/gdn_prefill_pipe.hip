@@ -438,10 +438,9 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
     wait_ge(&sm.cnt[CNT_DONE], (unsigned)(x >= 2 ? NSIG * (x - 1) : 0));
 #pragma unroll
     for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.kb[x & 1][4 * it + gq][swz(4 * it + gq, m * 8)]) = sk[it];
-    wait_ge(&sm.cnt[CNT_QVFREE], (unsigned)(NSIG * x));
-#pragma unroll
-    for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.qb[4 * it + gq][swz(4 * it + gq, m * 8)]) = sq[it];
-    // V rows of the workgroup's VB columns: VB / 8 lanes per row
+    // V rows of the workgroup's VB columns (VB / 8 lanes per row), loaded into
+    // the registers the K rows held, so that their latency overlaps the wait
+    // for the Q and V buffers
     constexpr int VLR = VB / 8, VRI = 64 / VLR, VIT = C / VRI;
     const int vr = lane / VLR, vsg = lane - vr * VLR;
     const uint16_t* vc0 = pc.v + (size_t)tb * pc.v_stride + (size_t)pc.h * D + pc.vcb0;
@@ -451,6 +450,9 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
         sv[it] = uint4{0, 0, 0, 0};
         sv[it] = ld16(vc0, 2u * ((unsigned)min(VRI * it + vr, L - 1) * (unsigned)pc.v_stride + 8u * vsg));
     }
+    wait_ge(&sm.cnt[CNT_QVFREE], (unsigned)(NSIG * x));
+#pragma unroll
+    for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.qb[4 * it + gq][swz(4 * it + gq, m * 8)]) = sq[it];
 #pragma unroll
     for (int it = 0; it < VIT; ++it)
         *reinterpret_cast<uint4*>(&sm.vb[VRI * it + vr][swz(VRI * it + vr, 8 * vsg)]) = sv[it];
