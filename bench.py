@@ -251,7 +251,8 @@ def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=50,
+                    help="untimed warm-up steps; the clocks settle after about 20 steps of the default workload")
     ap.add_argument("--workload", default="decode_b64+prefill_varlen16",
                     choices=["decode_b64+prefill_varlen16", "decode_b64", "decode_sweep",
                              "prefill_varlen16", "prefill_long2x64k", "copy_calibration"])
