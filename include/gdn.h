@@ -121,7 +121,8 @@ GDN_API size_t gdn_prefill_workspace_size(int N, int T, int H_qk, int H_v,
  *                  gdn_prefill_workspace_size(...) bytes, 256-byte aligned;
  *                  its contents are scratch (overwritten by each call).
  *
- * N = 0 is a no-op returning GDN_OK.
+ * N = 0 is a no-op returning GDN_OK.  Size limits (GDN_EINVAL otherwise):
+ * T * H_v <= 2^24 and N * H_v <= 2^30.
  */
 GDN_API int gdn_prefill_varlen(const void* q, const void* k, const void* v,
                        const float* g, const float* beta,

@@ -114,6 +114,7 @@ STATE_BYTES = 3 * 2 * 128 * 128 * 4
     (dict(ws=None), EWS, "workspace"),
     (dict(ws_bytes=100), EWS, "256 bytes needed"),
     (dict(ws=P + 16), EALIGN, "workspace"),
+    (dict(T=1 << 20, H_qk=16, H_v=32), EINVAL, "problem too large"),
 ])
 def test_prefill_rejects(lib, kw, status, msg):
     assert prefill(lib, **kw) == status
