@@ -123,6 +123,42 @@ class Decode:
             self.i += 1
 
 
+class MultiToken:
+    """A multi-token decode step through gdn_prefill_varlen: ``N`` sequences of
+    ``len`` new tokens each, states updated in place (initial_state is
+    final_state).  ``per_step`` launches per call, each on the next of ``nbuf``
+    state buffers, as for Decode."""
+
+    def __init__(self, dev, w, nbuf=4, per_step=4):
+        import torch
+        from paper_2607_17979_amd import gdn
+        from paper_2607_17979_amd import workloads as wl
+
+        self.N, self.Tn, self.H_qk, self.H_v, self.D = w["N"], w["len"], w["H_qk"], w["H_v"], w["D"]
+        self.T = self.N * self.Tn
+        self.host = wl.prefill_inputs(w["seed"], [self.Tn] * self.N, self.H_qk, self.H_v, self.D,
+                                      state_std=w["state_std"])
+        self.x = _dev_inputs_prefill(self.host, dev)
+        self.states = [wl.to_torch(self.host.initial_state, dev) for _ in range(nbuf)]
+        self.o = torch.empty((self.T, self.H_v, self.D), dtype=torch.bfloat16, device=dev)
+        ws = gdn.gdn_prefill_workspace_size(self.N, self.T, self.H_qk, self.H_v, self.D, self.D, w["chunk"])
+        self.ws = torch.empty(max(ws, 256), dtype=torch.uint8, device=dev)
+        self.chunk = w["chunk"]
+        self.i = 0
+        self.per_step = per_step
+        self.bytes = prefill_bytes(self.T, self.N, self.H_qk, self.H_v, self.D, True)
+
+    def __call__(self):
+        from paper_2607_17979_amd import gdn
+
+        x = self.x
+        for _ in range(self.per_step):
+            st = self.states[self.i % len(self.states)]
+            gdn.gdn_prefill_varlen(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], st, st, self.o,
+                                   chunk=self.chunk, workspace=self.ws)
+            self.i += 1
+
+
 class Prefill:
     def __init__(self, dev, lengths, H_qk, H_v, D, C, seed, state_std):
         import torch
@@ -255,7 +291,8 @@ def main(argv=None):
                     help="untimed warm-up steps; the clocks settle after about 20 steps of the default workload")
     ap.add_argument("--workload", default="decode_b64+prefill_varlen16",
                     choices=["decode_b64+prefill_varlen16", "decode_b64", "decode_sweep",
-                             "prefill_varlen16", "prefill_long2x64k", "copy_calibration"])
+                             "prefill_varlen16", "prefill_long2x64k", "decode_multitoken",
+                             "copy_calibration"])
     ap.add_argument("--batch", type=int, default=None, help="decode_sweep: one batch size only")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args(argv)
@@ -311,6 +348,24 @@ def main(argv=None):
                       w["state_std"])
         parts.append(pre)
         names.append("prefill")
+
+    if args.workload == "decode_multitoken":
+        mt = MultiToken(dev, W["decode_multitoken"])
+        ms_step, per = _time_parts([mt], args.steps, args.warmup)
+        t = per[0] * 1e-3 / mt.per_step
+        gbs = mt.bytes / t / 1e9
+        out.update(value=gbs, unit="GB/s", ms_per_step=ms_step, dtype="f32",
+                   tokens_per_s=mt.T / t, us_per_launch=t * 1e6,
+                   roofline=dict(bound="hbm", achieved=gbs, peak=HBM_PEAK_GBS, unit="GB/s",
+                                 frac=gbs / HBM_PEAK_GBS, traffic=None,
+                                 kernel="gdn::recur::prefill_recur_kernel (token by token; "
+                                        "sequences of at most 8 tokens)",
+                                 bytes_per_launch=mt.bytes),
+                   config=dict(workload="decode_multitoken", N=mt.N, tokens_per_sequence=mt.Tn,
+                               H_qk=mt.H_qk, H_v=mt.H_v, d=mt.D, state_buffers=len(mt.states),
+                               launches_per_step=mt.per_step, in_place=True))
+        print(json.dumps(out), flush=True)
+        return 0
 
     if args.workload == "decode_sweep":
         w = W["decode_sweep"]

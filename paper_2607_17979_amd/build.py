@@ -13,7 +13,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB_NAME = "libgdn_mi355x.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
-SOURCES = ["csrc/gdn_api.cpp", "csrc/gdn_decode.hip", "csrc/gdn_prefill.hip", "csrc/gdn_prefill_pipe.hip"]
+SOURCES = ["csrc/gdn_api.cpp", "csrc/gdn_decode.hip", "csrc/gdn_prefill.hip", "csrc/gdn_prefill_pipe.hip",
+           "csrc/gdn_recur.hip"]
 ARCH = "gfx950"
 
 

@@ -37,9 +37,18 @@ struct PrefillArgs {
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
 hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream);
+// d = 128: sequences of at most kRecurMax tokens run token by token
+// (gdn_recur.hip), longer ones in chunks; the route depends only on a
+// sequence's own length.  The recurrent launch also writes the schedule.
+// Measured on 64 sequences x 32 heads: token by token is faster up to about
+// 10 tokens, the chunk kernel beyond.
+constexpr int kRecurMax = 8;
+hipError_t launch_prefill_recur(const PrefillArgs& a, int32_t* order, hipStream_t stream);
 // d = 128, chunk 64: the pipelined kernel (gdn_prefill_pipe.hip); `order` is the
 // longest-first schedule already written to the workspace.
 hipError_t launch_prefill_pipe(const PrefillArgs& a, const int32_t* order, hipStream_t stream);
+// Compute units of the current device (queried once per device).
+int device_compute_units();
 
 // Workspace layout of the prefill: int32 order[N] (sequence indices sorted by
 // length, longest first, ties by index), rounded up to 256 bytes.

@@ -34,6 +34,7 @@
 //     of two 16-row tiles, and the matching A operand is read from LDS in the
 //     same permuted contraction order (two 8-byte reads per lane).
 #include "gdn_launch.h"
+#include "gdn_schedule.h"
 #include "gdn_mfma.h"
 
 namespace gdn {
@@ -83,26 +84,10 @@ struct Smem {
 };
 
 // --- schedule: sequences by length, longest first (ties by index) ---------------
-constexpr int kSortMax = 4096;
-
 __global__ __launch_bounds__(256) void prefill_schedule_kernel(const int32_t* __restrict__ cu,
                                                                int N, int32_t* __restrict__ order) {
     __shared__ int len[kSortMax];
-    if (N > kSortMax) {
-        for (int i = threadIdx.x; i < N; i += blockDim.x) order[i] = i;
-        return;
-    }
-    for (int i = threadIdx.x; i < N; i += blockDim.x) len[i] = cu[i + 1] - cu[i];
-    __syncthreads();
-    for (int i = threadIdx.x; i < N; i += blockDim.x) {
-        const int li = len[i];
-        int rank = 0;
-        for (int j = 0; j < N; ++j) {
-            const int lj = len[j];
-            rank += (lj > li) || (lj == li && j < i);
-        }
-        order[rank] = i;
-    }
+    schedule_longest_first(cu, N, order, len);
 }
 
 // --- the chunk kernel ----------------------------------------------------------
@@ -491,10 +476,16 @@ size_t prefill_workspace_bytes(int N) {
 
 hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {
     int32_t* order = static_cast<int32_t*>(a.workspace);
+    if (a.D == 128) {
+        // short sequences token by token (that launch also writes the
+        // schedule), the rest in chunks; with T <= kRecurMax every sequence is short
+        hipError_t e = launch_prefill_recur(a, order, stream);
+        if (e != hipSuccess || a.T <= kRecurMax) return e;
+        return launch_prefill_pipe(a, order, stream);
+    }
     hipLaunchKernelGGL(prefill_schedule_kernel, dim3(1), dim3(256), 0, stream, a.cu_seqlens, a.N, order);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (a.D == 128) return launch_prefill_pipe(a, order, stream);
     typedef Cfg<16, 16> P16;
     hipLaunchKernelGGL((prefill_kernel<16, 16>), dim3((unsigned)(a.N * a.H_v)), dim3(P16::NT), 0,
                        stream, (const uint16_t*)a.q, (const uint16_t*)a.k, (const uint16_t*)a.v, a.g,

@@ -506,7 +506,8 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
         it.hq = it.h / (H_v / H_qk);
         it.seq_beg = cu[it.n];
         it.seq_len = cu[it.n + 1] - it.seq_beg;
-        it.nch = (it.seq_len + C - 1) / C;
+        // sequences of at most kRecurMax tokens belong to the recurrent kernel
+        it.nch = it.seq_len <= kRecurMax ? 0 : (it.seq_len + C - 1) / C;
         return it;
     };
     const size_t qk_stride = (size_t)H_qk * D;
@@ -556,6 +557,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
         const int item = item_at(pass);
         if (item < 0) break;
         const Item it = decode(item);
+        if (it.nch == 0) continue;  // a short sequence: the recurrent kernel's
         const int h = it.h, seq_beg = it.seq_beg, seq_len = it.seq_len, nch = it.nch;
         const size_t state_off = ((size_t)it.n * H_v + h) * D * D;
         const int vcol0 = (it.vblock * NS + wave) * VW;
@@ -941,8 +943,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
 
 }  // namespace pipe
 
-// Compute units of the current device (queried once per device).
-static int compute_units() {
+int device_compute_units() {
     static int cache[64] = {0};
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
@@ -959,7 +960,7 @@ template <int NS, int NVT, int NO>
 static hipError_t launch_pipe(const PrefillArgs& a, const int32_t* order, hipStream_t stream) {
     constexpr int VSPLIT = pipe::D / (16 * NS * NVT);
     const long items = (long)a.N * a.H_v * VSPLIT;
-    const long grid = std::min<long>(items, compute_units());
+    const long grid = std::min<long>(items, device_compute_units());
     hipLaunchKernelGGL((pipe::prefill_pipe_kernel<NS, NVT, NO>), dim3((unsigned)grid),
                        dim3(64 * (NS + NO + pipe::NP)), 0, stream, (const uint16_t*)a.q, (const uint16_t*)a.k,
                        (const uint16_t*)a.v, a.g, a.beta, a.cu_seqlens, order, a.initial_state, a.final_state,
@@ -972,7 +973,7 @@ static hipError_t launch_pipe(const PrefillArgs& a, const int32_t* order, hipStr
 // workgroups (one workgroup per compute unit fits in LDS).
 hipError_t launch_prefill_pipe(const PrefillArgs& a, const int32_t* order, hipStream_t stream) {
     const long heads = (long)a.N * a.H_v;
-    const long cus = compute_units();
+    const long cus = device_compute_units();
     if (heads * 4 <= cus) return launch_pipe<2, 1, 2>(a, order, stream);
     if (heads * 2 <= cus) return launch_pipe<4, 1, 0>(a, order, stream);
     return launch_pipe<4, 2, 0>(a, order, stream);

@@ -1,0 +1,181 @@
+// Short sequences of the prefill regime, token by token (paper: appendix
+// "Operator Background and Mathematical Definitions", subsection "Gated Delta
+// Net": the recurrence applied to each new token in turn), for d = 128.
+//
+// For a sequence of a few tokens the chunk kernel pays a whole chunk (the
+// producer's start-up, a state load, one pass of the state chain) and its
+// per-item costs dominate; token by token such a sequence costs one pass over
+// its state plus a few rank-1 updates.  This kernel runs every sequence of
+// 0 .. kRecurMax tokens and the chunk kernel skips them, so the route of a
+// sequence depends only on its own length, never on the rest of the batch.
+// With initial_state == final_state this is also the multi-token decode of a
+// batch (each sequence a few new tokens, states updated in place).
+//
+// Per (sequence, value head), state row i and token t, alpha_t = exp(g_t):
+//     kv_i = S_i . k_t,  sq_i = S_i . q_t                  (row before the token)
+//     u_i  = beta_t (v_{t,i} - alpha_t kv_i)
+//     S_i  = alpha_t S_i + u_i k_t^T
+//     o_{t,i} = scale (alpha_t sq_i + u_i (k_t . q_t))      (= scale S_t q_t)
+// Rows are independent, so a workgroup keeps 32 rows of one (sequence, head)
+// in registers for the whole sequence, in the decode kernel's layout (a row of
+// 128 fp32 over 8 consecutive lanes, 16 values per lane; S k and S q are sums
+// over those 8 lanes).  The sequence's token inputs are staged in LDS first.
+//
+// Block 0 writes the longest-first schedule of the chunk kernel, which runs
+// after this one on the same stream: the schedule costs no launch of its own.
+#include <algorithm>
+
+#include "gdn_device.h"
+#include "gdn_launch.h"
+#include "gdn_schedule.h"
+
+namespace gdn {
+namespace recur {
+
+constexpr int D = 128;
+constexpr int LPR = 8;                        // lanes per state row
+constexpr int J = D / (4 * LPR);              // float4 slots per lane
+constexpr int ROWS_PER_WAVE = 64 / LPR;
+constexpr int NWAVE = 4;
+constexpr int BPH = D / (NWAVE * ROWS_PER_WAVE);  // workgroups per (sequence, head)
+
+// A unit's token inputs, staged in LDS once (their latency paid once per
+// unit, not per token): k and q rows of the q/k head widened to fp32, this
+// workgroup's 32 values of v, alpha = exp(g), beta and k . q per token.  Block
+// 0 uses the same LDS for the schedule.
+union Smem {
+    int sched_len[kSortMax];
+    struct {
+        alignas(16) float k[kRecurMax][D];
+        alignas(16) float q[kRecurMax][D];
+        uint16_t v[kRecurMax][NWAVE * ROWS_PER_WAVE];
+        float alpha[kRecurMax], b[kRecurMax], kq[kRecurMax];
+    } tok;
+};
+
+__global__ __launch_bounds__(256) void prefill_recur_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+    const float* __restrict__ g, const float* __restrict__ beta, const int32_t* __restrict__ cu,
+    int32_t* __restrict__ order, const float* initial_state, float* final_state,
+    uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale) {
+    __shared__ Smem sm;
+    if (blockIdx.x == 0) {
+        schedule_longest_first(cu, N, order, sm.sched_len);
+        return;
+    }
+    constexpr int ROWS = NWAVE * ROWS_PER_WAVE;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int sub = lane / LPR, c = lane % LPR;
+    const long units = (long)N * H_v * BPH;
+    const size_t qk_stride = (size_t)H_qk * D, v_stride = (size_t)H_v * D;
+    for (long u = blockIdx.x - 1; u < units; u += gridDim.x - 1) {
+        const long head = u / BPH;  // n H_v + h
+        const int blk = (int)(u - head * BPH);
+        const int n = (int)(head / H_v);
+        const int h = (int)(head - (long)n * H_v);
+        const int hq = h / (H_v / H_qk);
+        const int t0 = cu[n];
+        const int len = cu[n + 1] - t0;
+        if (len > kRecurMax) continue;  // the chunk kernel's
+        const int row0 = blk * ROWS;
+        const int row = row0 + wave * ROWS_PER_WAVE + sub;
+        const size_t srow = ((size_t)head * D + row) * D;
+        f32x4_t s[J];
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            if (initial_state != nullptr)
+                s[j] = __builtin_nontemporal_load(
+                    reinterpret_cast<const f32x4_t*>(initial_state + srow + (j * LPR + c) * 4));
+            else
+                s[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        }
+        // stage the tokens: 16 segments of 8 values per k or q row, 4 per v slice
+        if (tid < len * (D / 8)) {
+            const int t = tid / (D / 8), seg = tid - t * (D / 8);
+            const size_t src = (size_t)(t0 + t) * qk_stride + (size_t)hq * D + seg * 8;
+            const uint4 kk = *reinterpret_cast<const uint4*>(k + src);
+            const uint4 qq = *reinterpret_cast<const uint4*>(q + src);
+            const uint32_t kw[4] = {kk.x, kk.y, kk.z, kk.w}, qw[4] = {qq.x, qq.y, qq.z, qq.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                sm.tok.k[t][seg * 8 + 2 * e] = bf16_to_f32(kw[e] & 0xFFFF);
+                sm.tok.k[t][seg * 8 + 2 * e + 1] = bf16_to_f32(kw[e] >> 16);
+                sm.tok.q[t][seg * 8 + 2 * e] = bf16_to_f32(qw[e] & 0xFFFF);
+                sm.tok.q[t][seg * 8 + 2 * e + 1] = bf16_to_f32(qw[e] >> 16);
+            }
+        }
+        if (tid < len * (ROWS / 8)) {
+            const int t = tid / (ROWS / 8), seg = tid - t * (ROWS / 8);
+            *reinterpret_cast<uint4*>(&sm.tok.v[t][seg * 8]) =
+                *reinterpret_cast<const uint4*>(v + (size_t)(t0 + t) * v_stride + (size_t)h * D + row0 + seg * 8);
+        }
+        if (tid < len) {
+            sm.tok.alpha[tid] = fast_exp(g[(size_t)(t0 + tid) * H_v + h]);
+            sm.tok.b[tid] = beta[(size_t)(t0 + tid) * H_v + h];
+        }
+        __syncthreads();
+        // k . q per token, summed in the row layout below (8 tokens per wave)
+        if (tid < 8 * len) {
+            const int t = tid / LPR;
+            float kq = 0.f;
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                const f32x4_t kv4 = *reinterpret_cast<const f32x4_t*>(&sm.tok.k[t][(j * LPR + c) * 4]);
+                const f32x4_t qv4 = *reinterpret_cast<const f32x4_t*>(&sm.tok.q[t][(j * LPR + c) * 4]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) kq = fmaf(kv4[e], qv4[e], kq);
+            }
+            kq = group_sum<LPR>(kq);
+            if (c == 0) sm.tok.kq[t] = kq;
+        }
+        __syncthreads();
+        for (int t = 0; t < len; ++t) {
+            f32x4_t kf[J], qf[J];
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                kf[j] = *reinterpret_cast<const f32x4_t*>(&sm.tok.k[t][(j * LPR + c) * 4]);
+                qf[j] = *reinterpret_cast<const f32x4_t*>(&sm.tok.q[t][(j * LPR + c) * 4]);
+            }
+            const float alpha = sm.tok.alpha[t], bt = sm.tok.b[t], kq = sm.tok.kq[t];
+            float kv = 0.f, sq = 0.f;
+#pragma unroll
+            for (int j = 0; j < J; ++j)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    kv = fmaf(s[j][e], kf[j][e], kv);
+                    sq = fmaf(s[j][e], qf[j][e], sq);
+                }
+            kv = group_sum<LPR>(kv);
+            sq = group_sum<LPR>(sq);
+            const float uu = bt * (bf16_to_f32(sm.tok.v[t][row - row0]) - alpha * kv);
+#pragma unroll
+            for (int j = 0; j < J; ++j)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) s[j][e] = fmaf(alpha, s[j][e], uu * kf[j][e]);
+            if (c == 0)
+                o[(size_t)(t0 + t) * v_stride + (size_t)h * D + row] = f32_to_bf16(scale * fmaf(alpha, sq, uu * kq));
+        }
+#pragma unroll
+        for (int j = 0; j < J; ++j)
+            __builtin_nontemporal_store(s[j], reinterpret_cast<f32x4_t*>(final_state + srow + (j * LPR + c) * 4));
+        __syncthreads();  // the staged tokens are read; the next unit may overwrite them
+    }
+}
+
+}  // namespace recur
+
+// Up to eight workgroups per compute unit, each walking (sequence, head, row
+// block) units; block 0 writes the schedule.
+hipError_t launch_prefill_recur(const PrefillArgs& a, int32_t* order, hipStream_t stream) {
+    const long units = (long)a.N * a.H_v * recur::BPH;
+    const long grid = 1 + std::max<long>(1, std::min<long>(units, 8L * device_compute_units()));
+    hipLaunchKernelGGL(recur::prefill_recur_kernel, dim3((unsigned)grid), dim3(64 * recur::NWAVE), 0, stream,
+                       (const uint16_t*)a.q, (const uint16_t*)a.k, (const uint16_t*)a.v, a.g, a.beta,
+                       a.cu_seqlens, order, a.initial_state, a.final_state, (uint16_t*)a.o, a.N, a.H_qk,
+                       a.H_v, a.scale);
+    return hipGetLastError();
+}
+
+}  // namespace gdn

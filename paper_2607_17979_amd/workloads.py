@@ -211,6 +211,9 @@ WORKLOADS = {
                              D=128, chunk=64, state_std=None, seed=4),
     "prefill_long2x64k": dict(kind="prefill", N=2, len=65536, H_qk=16, H_v=32, D=128, chunk=64,
                               state_std=0.02, seed=5),
+    # a multi-token decode step: 64 sequences with 4 new tokens each, states in place
+    "decode_multitoken": dict(kind="prefill", N=64, len=4, H_qk=16, H_v=32, D=128, chunk=64,
+                              state_std=0.02, seed=6),
 }
 
 

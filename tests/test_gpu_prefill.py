@@ -248,3 +248,78 @@ def test_prefill_several_items_per_workgroup():
         o1, f1 = _prefill_gpu(one, dev)
         assert torch.equal(o[a:b].view(torch.int16), o1.view(torch.int16)), n
         assert torch.equal(fin[n].view(torch.int32), f1[0].view(torch.int32)), n
+
+
+def test_prefill_short_sequences_token_by_token():
+    """Sequences of at most 8 tokens run token by token (the chunk kernel skips
+    them): lengths on both sides of that threshold, zero included, against the
+    oracle; a zero-length sequence keeps its initial state bit for bit."""
+    dev = device()
+    lengths = [0, 1, 2, 7, 8, 9, 15, 16, 31, 64, 65, 8, 3]
+    note(f"prefill short sequences {lengths}")
+    inp = wl.prefill_inputs(45, lengths, 2, 4, 128, state_std=0.02)
+    inp.scale = 128 ** -0.5
+    o, fin = _prefill_gpu(inp, dev)
+    _full_oracle_check(inp, o, fin, "short sequences")
+    assert np.array_equal(fin.cpu().numpy()[0], inp.initial_state[0])
+
+
+def test_prefill_short_route_zero_initial_state():
+    """Only short sequences (T <= 8: the chunk kernel is not launched), no
+    initial state."""
+    dev = device()
+    inp = wl.prefill_inputs(46, [3, 0, 5], 2, 4, 128)
+    note("prefill short route, T = 8, zero initial state")
+    o, fin = _prefill_gpu(inp, dev)
+    _full_oracle_check(inp, o, fin, "short route, zero state")
+
+
+def test_multi_token_decode_equals_decode_steps_bitwise():
+    """B sequences with Tn new tokens each and states updated in place (a
+    multi-token decode step) equal Tn gdn_decode calls bit for bit: the
+    token-by-token route applies the decode arithmetic per token.  Checked
+    against the oracle as well."""
+    import torch
+
+    dev = device()
+    B, Tn = 8, 4
+    note(f"multi-token decode B={B} Tn={Tn}")
+    inp = wl.prefill_inputs(47, [Tn] * B, 16, 32, 128, state_std=0.02)
+    o1, f1 = _prefill_gpu(inp, dev, in_place=True)
+    st = to_dev(inp.initial_state, dev)
+    outs = []
+    for t in range(Tn):
+        idx = np.arange(B) * Tn + t
+        q, k, v = (to_dev(x[idx], dev, bf16=True) for x in (inp.q, inp.k, inp.v))
+        o = torch.empty(v.shape, dtype=torch.bfloat16, device=dev)
+        gdn.gdn_decode(q, k, v, to_dev(inp.g[idx], dev), to_dev(inp.beta[idx], dev), st, o)
+        outs.append(o)
+    torch.cuda.synchronize()
+    o_dec = torch.stack(outs, dim=1).reshape(B * Tn, 32, 128)
+    assert torch.equal(o1.view(torch.int16), o_dec.view(torch.int16))
+    assert torch.equal(f1, st)
+    _full_oracle_check(inp, o1, f1, "multi-token decode")
+
+
+def test_prefill_many_short_sequences():
+    """The short-sequence regime at the bench's head layout: 64 sequences of
+    8 tokens, 32 value / 16 q/k heads, nonzero states (sampled units)."""
+    dev = device()
+    note("prefill 64 x 8 tokens")
+    inp = wl.prefill_inputs(48, [8] * 64, 16, 32, 128, state_std=0.02)
+    o, fin = _prefill_gpu(inp, dev)
+    units = [(n, (5 * n + 1) % 32) for n in range(64)] + [(3, h) for h in range(32)]
+    _sampled_check(inp, o, fin, units, "64 x 8")
+
+
+def test_decode_multitoken_workload_parity():
+    """The bench's multi-token decode step: 64 sequences x 4 new tokens, 32
+    value / 16 q/k heads, states updated in place (sampled units)."""
+    dev = device()
+    w = wl.WORKLOADS["decode_multitoken"]
+    note("multi-token decode workload 64 x 4, in place")
+    inp = wl.prefill_inputs(w["seed"], [w["len"]] * w["N"], w["H_qk"], w["H_v"], w["D"],
+                            state_std=w["state_std"])
+    o, fin = _prefill_gpu(inp, dev, in_place=True)
+    units = [(n, (3 * n + 5) % w["H_v"]) for n in range(w["N"])] + [(0, h) for h in range(w["H_v"])]
+    _sampled_check(inp, o, fin, units, "multi-token decode 64 x 4")
