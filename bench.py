@@ -420,7 +420,7 @@ def main(argv=None):
                     roofline=dict(bound="mfma", achieved=tflops, peak=BF16_PEAK_TFLOPS,
                                   unit="TFLOP/s", frac=tflops / BF16_PEAK_TFLOPS,
                                   traffic=measured_traffic("prefill_kernel"),
-                                  kernel="gdn::pipe::prefill_pipe_kernel<NS,NVT,NO> (+ schedule kernel; the launcher picks the variant from N*H_v and the CU count)",
+                                  kernel="gdn::pipe::prefill_pipe_kernel<NS,NVT,NO> (+ the token-by-token launch, which writes the schedule; the launcher picks the variant from N*H_v and the CU count)",
                                   flops_per_launch=pre.flops))
         out["prefill"] = pobj
         cfg["prefill"] = dict(N=pre.N, T=pre.T, H_qk=pre.H_qk, H_v=pre.H_v, d=pre.D, chunk=pre.C,

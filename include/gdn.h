@@ -91,7 +91,8 @@ GDN_API int gdn_decode(const void* q, const void* k, const void* v,
 
 /*
  * Bytes of device workspace gdn_prefill_varlen needs for N sequences (the
- * longest-first schedule: one int32 per sequence, rounded up to 256 bytes).
+ * longest-first schedule, one int32 per sequence, and one int32 count of the
+ * sequences run in chunks; rounded up to 256 bytes).
  * Returns 0 for invalid arguments.
  */
 GDN_API size_t gdn_prefill_workspace_size(int N, int T, int H_qk, int H_v,
@@ -120,6 +121,14 @@ GDN_API size_t gdn_prefill_workspace_size(int N, int T, int H_qk, int H_v,
  *   workspace      device buffer of at least
  *                  gdn_prefill_workspace_size(...) bytes, 256-byte aligned;
  *                  its contents are scratch (overwritten by each call).
+ *
+ * For D = 128, sequences of at most 8 tokens are computed token by token in
+ * fp32 (the decode arithmetic), longer ones in chunks; the choice depends
+ * only on each sequence's own length, so a sequence's result does not depend
+ * on the rest of the batch.  With initial_state == final_state and short
+ * sequences this call is a multi-token decode step (n new tokens per
+ * sequence, cu_seqlens = [0, n, 2n, ...]); for n <= 8 it equals n calls of
+ * gdn_decode bit for bit.
  *
  * N = 0 is a no-op returning GDN_OK.  Size limits (GDN_EINVAL otherwise):
  * T * H_v <= 2^24 and N * H_v <= 2^30.

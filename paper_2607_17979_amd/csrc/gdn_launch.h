@@ -51,7 +51,8 @@ hipError_t launch_prefill_pipe(const PrefillArgs& a, const int32_t* order, hipSt
 int device_compute_units();
 
 // Workspace layout of the prefill: int32 order[N] (sequence indices sorted by
-// length, longest first, ties by index), rounded up to 256 bytes.
+// length, longest first, ties by index), then (d = 128) int32 order[N] = the
+// number of sequences longer than kRecurMax; rounded up to 256 bytes.
 size_t prefill_workspace_bytes(int N);
 
 }  // namespace gdn

@@ -477,6 +477,8 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
     static_assert(NO == 0 || NO == NS, "one output wave per state wave");
     __shared__ Smem<VB, NO, NVT> sm;
 
+    // no sequence longer than kRecurMax: all of them ran token by token
+    if (order[N] == 0) return;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar chunk and address math

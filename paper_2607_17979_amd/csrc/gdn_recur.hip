@@ -22,7 +22,9 @@
 // over those 8 lanes).  The sequence's token inputs are staged in LDS first.
 //
 // Block 0 writes the longest-first schedule of the chunk kernel, which runs
-// after this one on the same stream: the schedule costs no launch of its own.
+// after this one on the same stream (the schedule costs no launch of its
+// own), and the number of sequences left to it, so that it exits at once
+// when every sequence is short.
 #include <algorithm>
 
 #include "gdn_device.h"
@@ -59,8 +61,17 @@ __global__ __launch_bounds__(256) void prefill_recur_kernel(
     int32_t* __restrict__ order, const float* initial_state, float* final_state,
     uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale) {
     __shared__ Smem sm;
+    __shared__ int nlong;
     if (blockIdx.x == 0) {
+        // the chunk kernel's schedule, then the number of sequences it runs
         schedule_longest_first(cu, N, order, sm.sched_len);
+        if (threadIdx.x == 0) nlong = 0;
+        __syncthreads();
+        int mine = 0;
+        for (int i = threadIdx.x; i < N; i += blockDim.x) mine += cu[i + 1] - cu[i] > kRecurMax;
+        if (mine) atomicAdd(&nlong, mine);
+        __syncthreads();
+        if (threadIdx.x == 0) order[N] = nlong;
         return;
     }
     constexpr int ROWS = NWAVE * ROWS_PER_WAVE;

@@ -150,8 +150,8 @@ def test_prefill_gva_equals_repeated_heads_bitwise():
 
 
 def test_prefill_schedule_is_longest_first():
-    """The workspace holds the sequence order, longest first, ties by index
-    (integer work: compared exactly)."""
+    """The workspace holds the sequence order, longest first, ties by index,
+    then the count of sequences run in chunks (integer work: compared exactly)."""
     import torch
 
     dev = device()
@@ -160,9 +160,11 @@ def test_prefill_schedule_is_longest_first():
     ws = torch.zeros(256, dtype=torch.uint8, device=dev)
     _prefill_gpu(inp, dev, workspace=ws)
     torch.cuda.synchronize()
-    order = ws.view(torch.int32)[:len(lengths)].cpu().numpy()
+    words = ws.view(torch.int32)[:len(lengths) + 1].cpu().numpy()
     expect = sorted(range(len(lengths)), key=lambda i: (-lengths[i], i))
-    assert order.tolist() == expect
+    assert words[:-1].tolist() == expect
+    # then the number of sequences run in chunks (longer than 8 tokens)
+    assert words[-1] == sum(n > 8 for n in lengths)
 
 
 def test_prefill_then_decode_continues_the_sequence():
