@@ -123,6 +123,38 @@ class Decode:
             self.i += 1
 
 
+class DecodeIndexed:
+    """``per_step`` gdn_decode_indexed launches per call on a pool of
+    ``nbuf`` x B slots: launch i updates the B distinct slots of index set
+    i % nbuf (the index sets are disjoint shuffles of the pool), so, as for
+    Decode, successive launches stream their states from HBM."""
+
+    def __init__(self, dev, B, H_qk, H_v, D, seed, nbuf=4, per_step=4):
+        import numpy as np
+        import torch
+        from paper_2607_17979_amd import workloads as wl
+
+        self.B, self.H_qk, self.H_v, self.D = B, H_qk, H_v, D
+        self.host = wl.decode_inputs(seed, B, H_qk, H_v, D)
+        self.x = _dev_inputs_decode(self.host, dev)
+        self.pool = torch.cat([wl.to_torch(self.host.state, dev) for _ in range(nbuf)])
+        perm = np.random.default_rng(seed).permutation(nbuf * B).astype(np.int32)
+        self.idx = [torch.as_tensor(perm[i * B:(i + 1) * B], device=dev) for i in range(nbuf)]
+        self.o = torch.empty((B, H_v, D), dtype=torch.bfloat16, device=dev)
+        self.i = 0
+        self.per_step = per_step
+        self.bytes = decode_bytes(B, H_qk, H_v, D) + 4 * B
+
+    def __call__(self):
+        from paper_2607_17979_amd import gdn
+
+        x = self.x
+        for _ in range(self.per_step):
+            gdn.gdn_decode_indexed(x["q"], x["k"], x["v"], x["g"], x["beta"], self.pool,
+                                   self.idx[self.i % len(self.idx)], self.o)
+            self.i += 1
+
+
 class MultiToken:
     """A multi-token decode step through gdn_prefill_varlen: ``N`` sequences of
     ``len`` new tokens each, states updated in place (initial_state is
@@ -292,7 +324,7 @@ def main(argv=None):
     ap.add_argument("--workload", default="decode_b64+prefill_varlen16",
                     choices=["decode_b64+prefill_varlen16", "decode_b64", "decode_sweep",
                              "prefill_varlen16", "prefill_long2x64k", "decode_multitoken",
-                             "copy_calibration"])
+                             "decode_indexed", "copy_calibration"])
     ap.add_argument("--batch", type=int, default=None, help="decode_sweep: one batch size only")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args(argv)
@@ -348,6 +380,21 @@ def main(argv=None):
                       w["state_std"])
         parts.append(pre)
         names.append("prefill")
+
+    if args.workload == "decode_indexed":
+        w = W["decode_b64"]
+        di = DecodeIndexed(dev, w["B"], w["H_qk"], w["H_v"], w["D"], w["seed"])
+        ms_step, per = _time_parts([di], args.steps, args.warmup)
+        t = per[0] * 1e-3 / di.per_step
+        gbs = di.bytes / t / 1e9
+        out.update(value=gbs, unit="GB/s", ms_per_step=ms_step, dtype="f32", us_per_launch=t * 1e6,
+                   roofline=dict(bound="hbm", achieved=gbs, peak=HBM_PEAK_GBS, unit="GB/s",
+                                 frac=gbs / HBM_PEAK_GBS, traffic=None,
+                                 kernel="gdn::decode_kernel<128,1,true>", bytes_per_launch=di.bytes),
+                   config=dict(workload="decode_indexed", B=di.B, pool_slots=int(di.pool.shape[0]),
+                               H_qk=di.H_qk, H_v=di.H_v, d=di.D, launches_per_step=di.per_step))
+        print(json.dumps(out), flush=True)
+        return 0
 
     if args.workload == "decode_multitoken":
         mt = MultiToken(dev, W["decode_multitoken"])

@@ -90,6 +90,32 @@ GDN_API int gdn_decode(const void* q, const void* k, const void* v,
                float scale, void* stream);
 
 /*
+ * gdn_decode_indexed -- gdn_decode on states kept in a pool of P slots, as a
+ * server keeps one state per request rather than per batch position: batch
+ * entry b updates slot state_idx[b].
+ *
+ *   state_pool  fp32 [P, H_v, D, D]  the slots named in state_idx are read,
+ *                                    then overwritten IN PLACE; others untouched
+ *   state_idx   int32 [B], device    slot of each batch entry.  Entries outside
+ *                                    [0, P) are skipped (their state and o rows
+ *                                    are not touched), so -1 marks padding.
+ *                                    Slots must be distinct within one call
+ *                                    (a repeated slot is a data race).  The
+ *                                    library never reads it on the host.
+ *   P           number of slots
+ *
+ * The other arguments are those of gdn_decode.  B = 0 or P = 0 is a no-op
+ * returning GDN_OK.  Errors as gdn_decode, plus GDN_EINVAL for P < 0, a NULL
+ * state_idx or P * H_v > 2^30, GDN_EALIGN for a state_idx that is not 4-byte
+ * aligned.
+ */
+GDN_API int gdn_decode_indexed(const void* q, const void* k, const void* v,
+               const float* g, const float* beta,
+               float* state_pool, const int32_t* state_idx, void* o,
+               int B, int P, int H_qk, int H_v, int D_k, int D_v,
+               float scale, void* stream);
+
+/*
  * Bytes of device workspace gdn_prefill_varlen needs for N sequences (the
  * longest-first schedule, one int32 per sequence, and one int32 count of the
  * sequences run in chunks; rounded up to 256 bytes).

@@ -73,7 +73,30 @@ int gdn_decode(const void* q, const void* k, const void* v, const float* g, cons
         (st = check_ptr16(state, "state")) || (st = check_ptr16(o, "o")) ||
         (st = check_ptr4(g, "g")) || (st = check_ptr4(beta, "beta")))
         return st;
-    gdn::DecodeArgs a{q, k, v, g, beta, state, o, B, H_qk, H_v, D_k, scale};
+    gdn::DecodeArgs a{q, k, v, g, beta, state, o, B, H_qk, H_v, D_k, scale, nullptr, 0};
+    hipError_t e = gdn::launch_decode(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(GDN_EHIP, "decode launch failed: %s", hipGetErrorString(e));
+    return GDN_OK;
+}
+
+int gdn_decode_indexed(const void* q, const void* k, const void* v, const float* g, const float* beta,
+                       float* state_pool, const int32_t* state_idx, void* o, int B, int P, int H_qk,
+                       int H_v, int D_k, int D_v, float scale, void* stream) {
+    g_last_error.clear();
+    if (B < 0) return fail(GDN_EINVAL, "B must be >= 0 (got %d)", B);
+    if (P < 0) return fail(GDN_EINVAL, "P must be >= 0 (got %d)", P);
+    if (int st = check_heads(H_qk, H_v, D_k, D_v)) return st;
+    if (B == 0 || P == 0) return GDN_OK;
+    if ((long long)B * H_v > (1LL << 30))
+        return fail(GDN_EINVAL, "B * H_v = %lld too large", (long long)B * H_v);
+    if ((long long)P * H_v > (1LL << 30))
+        return fail(GDN_EINVAL, "P * H_v = %lld too large", (long long)P * H_v);
+    int st;
+    if ((st = check_ptr16(q, "q")) || (st = check_ptr16(k, "k")) || (st = check_ptr16(v, "v")) ||
+        (st = check_ptr16(state_pool, "state_pool")) || (st = check_ptr4(state_idx, "state_idx")) ||
+        (st = check_ptr16(o, "o")) || (st = check_ptr4(g, "g")) || (st = check_ptr4(beta, "beta")))
+        return st;
+    gdn::DecodeArgs a{q, k, v, g, beta, state_pool, o, B, H_qk, H_v, D_k, scale, state_idx, P};
     hipError_t e = gdn::launch_decode(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail(GDN_EHIP, "decode launch failed: %s", hipGetErrorString(e));
     return GDN_OK;

@@ -26,12 +26,15 @@
 
 namespace gdn {
 
-template <int D, int RS>
+// INDEXED: the state of batch entry b is pool slot idx[b] (entries outside
+// [0, P) are skipped) instead of state b.
+template <int D, int RS, bool INDEXED>
 __global__ __launch_bounds__(256) void decode_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const uint16_t* __restrict__ v, const float* __restrict__ g,
     const float* __restrict__ beta, float* __restrict__ state,
-    uint16_t* __restrict__ o, int H_qk, int H_v, int blocks_per_head, float scale) {
+    uint16_t* __restrict__ o, int H_qk, int H_v, int blocks_per_head, float scale,
+    const int32_t* __restrict__ idx, int P) {
     constexpr int F4_ROW = D / 4;
     constexpr int LPR = F4_ROW < 8 ? F4_ROW : 8;
     constexpr int J = F4_ROW / LPR;
@@ -46,6 +49,12 @@ __global__ __launch_bounds__(256) void decode_kernel(
     const int b = head / H_v;
     const int h = head - b * H_v;
     const int hq = h / (H_v / H_qk);
+    long shead = head;  // (state slot) H_v + h
+    if constexpr (INDEXED) {
+        const int slot = idx[b];
+        if (slot < 0 || slot >= P) return;
+        shead = (long)slot * H_v + h;
+    }
     const int row0 = (blk * nwave + wave) * ROWS_PER_WAVE;
     const int sub = lane / LPR;
     const int c = lane % LPR;
@@ -71,7 +80,7 @@ __global__ __launch_bounds__(256) void decode_kernel(
 
     const float alpha = fast_exp(g[head]);
     const float bt = beta[head];
-    float* sp = state + (size_t)head * D * D;
+    float* sp = state + (size_t)shead * D * D;
     const uint16_t* vp = v + (size_t)head * D;
     uint16_t* op = o + (size_t)head * D;
 
@@ -130,9 +139,14 @@ static hipError_t launch_decode_d(const DecodeArgs& a, hipStream_t stream) {
     const int blocks_per_head = D / rows_per_block;
     const dim3 grid((unsigned)(heads * blocks_per_head));
     const dim3 block(64 * nwave);
-    hipLaunchKernelGGL((decode_kernel<D, 1>), grid, block, 0, stream, (const uint16_t*)a.q,
-                       (const uint16_t*)a.k, (const uint16_t*)a.v, a.g, a.beta, a.state,
-                       (uint16_t*)a.o, a.H_qk, a.H_v, blocks_per_head, a.scale);
+    if (a.state_idx != nullptr)
+        hipLaunchKernelGGL((decode_kernel<D, 1, true>), grid, block, 0, stream, (const uint16_t*)a.q,
+                           (const uint16_t*)a.k, (const uint16_t*)a.v, a.g, a.beta, a.state,
+                           (uint16_t*)a.o, a.H_qk, a.H_v, blocks_per_head, a.scale, a.state_idx, a.P);
+    else
+        hipLaunchKernelGGL((decode_kernel<D, 1, false>), grid, block, 0, stream, (const uint16_t*)a.q,
+                           (const uint16_t*)a.k, (const uint16_t*)a.v, a.g, a.beta, a.state,
+                           (uint16_t*)a.o, a.H_qk, a.H_v, blocks_per_head, a.scale, nullptr, 0);
     return hipGetLastError();
 }
 

@@ -18,6 +18,8 @@ struct DecodeArgs {
     void* o;
     int B, H_qk, H_v, D;
     float scale;
+    const int32_t* state_idx;  // NULL: state b is batch entry b; else a pool slot per entry
+    int P;                     // pool slots (with state_idx)
 };
 
 struct PrefillArgs {

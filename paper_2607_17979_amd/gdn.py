@@ -20,12 +20,13 @@ __all__ = [
     "gdn_last_error",
     "gdn_abi_version",
     "gdn_decode",
+    "gdn_decode_indexed",
     "gdn_prefill_workspace_size",
     "gdn_prefill_varlen",
     "EXPORTED_SYMBOLS",
 ]
 
-EXPORTED_SYMBOLS = ("gdn_last_error", "gdn_abi_version", "gdn_decode",
+EXPORTED_SYMBOLS = ("gdn_last_error", "gdn_abi_version", "gdn_decode", "gdn_decode_indexed",
                     "gdn_prefill_workspace_size", "gdn_prefill_varlen")
 
 _STATUS = {0: "GDN_OK", -1: "GDN_EINVAL", -2: "GDN_EUNSUPPORTED", -3: "GDN_EALIGN",
@@ -60,6 +61,8 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.gdn_abi_version.argtypes = []
     lib.gdn_decode.restype = ci
     lib.gdn_decode.argtypes = [vp, vp, vp, vp, vp, vp, vp, ci, ci, ci, ci, ci, cf, vp]
+    lib.gdn_decode_indexed.restype = ci
+    lib.gdn_decode_indexed.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, cf, vp]
     lib.gdn_prefill_workspace_size.restype = sz
     lib.gdn_prefill_workspace_size.argtypes = [ci, ci, ci, ci, ci, ci, ci]
     lib.gdn_prefill_varlen.restype = ci
@@ -132,6 +135,33 @@ def gdn_decode(q, k, v, g, beta, state, o, scale: float = 1.0, stream=None) -> N
     lib = load_library()
     _check(lib.gdn_decode(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(state), _ptr(o),
                           B, H_qk, H_v, D, D, float(scale), _stream(q, stream)))
+
+
+def gdn_decode_indexed(q, k, v, g, beta, state_pool, state_idx, o, scale: float = 1.0,
+                       stream=None) -> None:
+    """One decode step on pooled states (see include/gdn.h).  As gdn_decode,
+    with state_pool: fp32 [P, H_v, D, D] and state_idx: int32 [B] on the
+    device (slot of each batch entry; entries outside [0, P) are skipped)."""
+    import torch
+
+    B, H_qk, D = q.shape
+    H_v = v.shape[1]
+    P = state_pool.shape[0]
+    dev = q.device
+    if dev.type != "cuda":
+        raise ValueError("tensors must be on a GPU device")
+    _need(q, "q", torch.bfloat16, (B, H_qk, D), dev)
+    _need(k, "k", torch.bfloat16, (B, H_qk, D), dev)
+    _need(v, "v", torch.bfloat16, (B, H_v, D), dev)
+    _need(g, "g", torch.float32, (B, H_v), dev)
+    _need(beta, "beta", torch.float32, (B, H_v), dev)
+    _need(state_pool, "state_pool", torch.float32, (P, H_v, D, D), dev)
+    _need(state_idx, "state_idx", torch.int32, (B,), dev)
+    _need(o, "o", torch.bfloat16, (B, H_v, D), dev)
+    lib = load_library()
+    _check(lib.gdn_decode_indexed(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(state_pool),
+                                  _ptr(state_idx), _ptr(o), B, P, H_qk, H_v, D, D, float(scale),
+                                  _stream(q, stream)))
 
 
 def gdn_prefill_workspace_size(N: int, T: int, H_qk: int, H_v: int, D_k: int, D_v: int,

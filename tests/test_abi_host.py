@@ -86,6 +86,34 @@ def test_workspace_size(lib):
     assert ws_size(lib, N=-1) == 0
 
 
+def decode_indexed(lib, q=P, k=P, v=P, g=P, beta=P, pool=P, idx=P, o=P, B=2, Pn=4, H_qk=1, H_v=2,
+                   Dk=128, Dv=128, scale=1.0):
+    return lib.gdn_decode_indexed(q, k, v, g, beta, pool, idx, o, B, Pn, H_qk, H_v, Dk, Dv, scale, None)
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(B=-1), EINVAL, "B must be"),
+    (dict(Pn=-1), EINVAL, "P must be"),
+    (dict(H_qk=3, H_v=4), EINVAL, "multiple"),
+    (dict(Dk=64, Dv=64), EUNSUP, "head dim"),
+    (dict(idx=None), EINVAL, "state_idx is NULL"),
+    (dict(idx=P + 2), EALIGN, "state_idx"),
+    (dict(pool=None), EINVAL, "state_pool is NULL"),
+    (dict(pool=P + 4), EALIGN, "state_pool"),
+    (dict(Pn=1 << 30), EINVAL, "P * H_v"),
+    (dict(o=None), EINVAL, "o is NULL"),
+])
+def test_decode_indexed_rejects(lib, kw, status, msg):
+    assert decode_indexed(lib, **kw) == status
+    assert msg in gdn.gdn_last_error()
+
+
+def test_decode_indexed_empty_is_noop(lib):
+    assert decode_indexed(lib, q=None, k=None, v=None, g=None, beta=None, pool=None, idx=None, o=None,
+                          B=0) == OK
+    assert decode_indexed(lib, pool=None, idx=None, Pn=0) == OK
+
+
 def prefill(lib, q=P, k=P, v=P, g=P, beta=P, cu=P, init=None, fin=P, o=P, N=3, T=10, H_qk=1,
             H_v=2, Dk=128, Dv=128, chunk=64, ws=P, ws_bytes=256):
     return lib.gdn_prefill_varlen(q, k, v, g, beta, cu, init, fin, o, N, T, H_qk, H_v, Dk, Dv,

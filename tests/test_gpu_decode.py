@@ -238,3 +238,44 @@ def test_decode_graph_replay_matches_eager():
         assert torch.equal(s_graph, s_eager), f"state after replay {r}"
         for i, (a, b) in enumerate(zip(o_graph, o_eager)):
             assert torch.equal(a, b), f"output of step {i} after replay {r}"
+
+
+def test_decode_indexed_pool():
+    """Batch entries update the pool slots state_idx names: those slots and the
+    outputs equal gdn_decode on the gathered states bit for bit, and the
+    oracle; slots not named, and the output rows of entries whose index is
+    -1 or past the pool, are left untouched."""
+    import torch
+
+    dev = device()
+    B, P, H_qk, H_v, D = 64, 96, 16, 32, 128
+    note(f"decode indexed B={B} P={P}")
+    inp = wl.decode_inputs(60, B, H_qk, H_v, D, state_std=0.0)
+    rng = np.random.default_rng(61)
+    pool_host = (0.02 * rng.standard_normal((P, H_v, D, D))).astype(np.float32)
+    slots = rng.permutation(P)[:B].astype(np.int32)
+    slots[[3, 10]] = -1
+    slots[20] = P
+    valid = (slots >= 0) & (slots < P)
+    pool = to_dev(pool_host, dev)
+    q, k, v = (to_dev(x, dev, bf16=True) for x in (inp.q, inp.k, inp.v))
+    g, b = to_dev(inp.g, dev), to_dev(inp.beta, dev)
+    o = torch.full(v.shape, float("nan"), dtype=torch.bfloat16, device=dev)
+    gdn.gdn_decode_indexed(q, k, v, g, b, pool, to_dev(slots, dev), o)
+    # the same step with gdn_decode on the gathered states of the valid entries
+    vi = torch.as_tensor(np.nonzero(valid)[0], device=dev)
+    st = to_dev(pool_host[slots[valid]], dev)
+    o2 = torch.empty((int(valid.sum()), H_v, D), dtype=torch.bfloat16, device=dev)
+    gdn.gdn_decode(q[vi].contiguous(), k[vi].contiguous(), v[vi].contiguous(), g[vi].contiguous(),
+                   b[vi].contiguous(), st, o2)
+    torch.cuda.synchronize()
+    pool_np = pool.cpu().numpy()
+    assert np.array_equal(pool_np[slots[valid]], st.cpu().numpy())
+    assert torch.equal(o[vi].view(torch.int16), o2.view(torch.int16))
+    assert torch.isnan(o[torch.as_tensor(np.nonzero(~valid)[0], device=dev)].float()).all()
+    untouched = np.setdiff1d(np.arange(P), slots[valid])
+    assert np.array_equal(pool_np[untouched], pool_host[untouched])
+    o_ref, s_ref = ref.decode(inp.q[valid], inp.k[valid], inp.v[valid], inp.g[valid], inp.beta[valid],
+                              pool_host[slots[valid]])
+    check_outputs(bf16_np(o[vi]), o_ref, "indexed")
+    check_states(pool_np[slots[valid]], s_ref, "indexed")
