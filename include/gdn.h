@@ -169,6 +169,37 @@ GDN_API int gdn_prefill_varlen(const void* q, const void* k, const void* v,
                        void* workspace, size_t workspace_bytes,
                        void* stream);
 
+/*
+ * gdn_prefill_varlen_indexed -- gdn_prefill_varlen on states kept in a pool
+ * of P slots: sequence n starts from slot state_idx[n] and leaves its final
+ * state there (in place).  Serving code keeps one state per request; a new
+ * request's slot is zeroed by the caller first, and a few new tokens per
+ * sequence make this a multi-token decode step on pooled states.
+ *
+ *   state_pool  fp32 [P, H_v, D, D]  the slots named in state_idx are read,
+ *                                    then overwritten IN PLACE; others untouched
+ *   state_idx   int32 [N], device    slot of each sequence.  Sequences whose
+ *                                    entry is outside [0, P) are skipped: their
+ *                                    outputs are not written.  Slots must be
+ *                                    distinct within one call.  The library
+ *                                    never reads it on the host.
+ *   P           number of slots
+ *
+ * The other arguments are those of gdn_prefill_varlen (same workspace size,
+ * same routes).  N = 0 or P = 0 is a no-op returning GDN_OK.  Errors as
+ * gdn_prefill_varlen, plus GDN_EINVAL for P < 0, a NULL state_idx or
+ * P * H_v > 2^30, GDN_EALIGN for a state_idx that is not 4-byte aligned.
+ */
+GDN_API int gdn_prefill_varlen_indexed(const void* q, const void* k, const void* v,
+                       const float* g, const float* beta,
+                       const int32_t* cu_seqlens,
+                       float* state_pool, const int32_t* state_idx,
+                       void* o,
+                       int N, int T, int P, int H_qk, int H_v, int D_k, int D_v,
+                       int chunk, float scale,
+                       void* workspace, size_t workspace_bytes,
+                       void* stream);
+
 #ifdef __cplusplus
 }
 #endif

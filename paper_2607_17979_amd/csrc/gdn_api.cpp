@@ -146,7 +146,45 @@ int gdn_prefill_varlen(const void* q, const void* k, const void* v, const float*
                     workspace_bytes, workspace == nullptr ? " (NULL)" : "");
     if (!aligned(workspace, 256)) return fail(GDN_EALIGN, "workspace is not 256-byte aligned");
     gdn::PrefillArgs a{q, k, v, g, beta, cu_seqlens, initial_state, final_state, o,
-                       N, T, H_qk, H_v, D_k, chunk, scale, workspace};
+                       N, T, H_qk, H_v, D_k, chunk, scale, workspace, nullptr, 0};
+    hipError_t e = gdn::launch_prefill(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(GDN_EHIP, "prefill launch failed: %s", hipGetErrorString(e));
+    return GDN_OK;
+}
+
+int gdn_prefill_varlen_indexed(const void* q, const void* k, const void* v, const float* g,
+                               const float* beta, const int32_t* cu_seqlens, float* state_pool,
+                               const int32_t* state_idx, void* o, int N, int T, int P, int H_qk,
+                               int H_v, int D_k, int D_v, int chunk, float scale, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+    g_last_error.clear();
+    if (N < 0 || T < 0) return fail(GDN_EINVAL, "N and T must be >= 0 (N=%d, T=%d)", N, T);
+    if (P < 0) return fail(GDN_EINVAL, "P must be >= 0 (got %d)", P);
+    if (int st = check_heads(H_qk, H_v, D_k, D_v)) return st;
+    if (chunk != chunk_for(D_k))
+        return fail(GDN_EUNSUPPORTED, "chunk %d unsupported for head dim %d (use %d)", chunk, D_k,
+                    chunk_for(D_k));
+    if (N == 0 || P == 0) return GDN_OK;
+    if ((long long)T * H_v > (1LL << 31) / 128 || (long long)N * H_v > (1LL << 30))
+        return fail(GDN_EINVAL, "problem too large (N=%d, T=%d, H_v=%d)", N, T, H_v);
+    if ((long long)P * H_v > (1LL << 30))
+        return fail(GDN_EINVAL, "P * H_v = %lld too large", (long long)P * H_v);
+    int st;
+    if ((st = check_ptr4(cu_seqlens, "cu_seqlens")) || (st = check_ptr16(state_pool, "state_pool")) ||
+        (st = check_ptr4(state_idx, "state_idx")))
+        return st;
+    if (T > 0) {
+        if ((st = check_ptr16(q, "q")) || (st = check_ptr16(k, "k")) || (st = check_ptr16(v, "v")) ||
+            (st = check_ptr16(o, "o")) || (st = check_ptr4(g, "g")) || (st = check_ptr4(beta, "beta")))
+            return st;
+    }
+    const size_t need = gdn::prefill_workspace_bytes(N);
+    if (workspace == nullptr || workspace_bytes < need)
+        return fail(GDN_EWORKSPACE, "workspace of %zu bytes needed, %zu given%s", need,
+                    workspace_bytes, workspace == nullptr ? " (NULL)" : "");
+    if (!aligned(workspace, 256)) return fail(GDN_EALIGN, "workspace is not 256-byte aligned");
+    gdn::PrefillArgs a{q, k, v, g, beta, cu_seqlens, state_pool, state_pool, o,
+                       N, T, H_qk, H_v, D_k, chunk, scale, workspace, state_idx, P};
     hipError_t e = gdn::launch_prefill(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail(GDN_EHIP, "prefill launch failed: %s", hipGetErrorString(e));
     return GDN_OK;

@@ -35,6 +35,8 @@ struct PrefillArgs {
     int N, T, H_qk, H_v, D, chunk;
     float scale;
     void* workspace;
+    const int32_t* state_idx;  // NULL: state n is sequence n; else a pool slot per sequence
+    int P;                     // pool slots (with state_idx)
 };
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);

@@ -97,7 +97,8 @@ __global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
     const uint16_t* __restrict__ v, const float* __restrict__ g,
     const float* __restrict__ beta, const int32_t* __restrict__ cu,
     const int32_t* __restrict__ order, const float* initial_state, float* final_state,
-    uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale) {
+    uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale,
+    const int32_t* __restrict__ state_idx, int P_slots) {
     typedef Cfg<D, C> P;
     constexpr int KD = P::KD, KC = P::KC;
     typedef typename Frag<KD>::type FD;
@@ -118,11 +119,18 @@ __global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
     const int seq_beg = cu[n];
     const int seq_len = cu[n + 1] - seq_beg;
     const int vcol0 = wave * P::VW;
+    // the state of sequence n: state n, or pool slot state_idx[n] (outside the
+    // pool: the sequence is skipped)
+    long slot = n;
+    if (state_idx != nullptr) {
+        slot = state_idx[n];
+        if (slot < 0 || slot >= P_slots) return;
+    }
 
     // State S^T (d x v) for this wave's value columns, fp32 accumulators:
     // st[dt][vt][i] = S[v][d], v = vcol0 + 16 vt + m, d = 16 dt + 4 gq + i.
     f32x4_t st[P::NDT][P::NVT];
-    const size_t state_off = ((size_t)n * H_v + h) * D * D;
+    const size_t state_off = ((size_t)slot * H_v + h) * D * D;
 #pragma unroll
     for (int dt = 0; dt < P::NDT; ++dt)
 #pragma unroll
@@ -491,7 +499,7 @@ hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {
     hipLaunchKernelGGL((prefill_kernel<16, 16>), dim3((unsigned)(a.N * a.H_v)), dim3(P16::NT), 0,
                        stream, (const uint16_t*)a.q, (const uint16_t*)a.k, (const uint16_t*)a.v, a.g,
                        a.beta, a.cu_seqlens, (const int32_t*)order, a.initial_state, a.final_state,
-                       (uint16_t*)a.o, a.N, a.H_qk, a.H_v, a.scale);
+                       (uint16_t*)a.o, a.N, a.H_qk, a.H_v, a.scale, a.state_idx, a.P);
     return hipGetLastError();
 }
 

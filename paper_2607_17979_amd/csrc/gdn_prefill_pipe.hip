@@ -468,7 +468,8 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const float* __restrict__ g, const float* __restrict__ beta, const int32_t* __restrict__ cu,
     const int32_t* __restrict__ order, const float* initial_state, float* final_state,
-    uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale) {
+    uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale,
+    const int32_t* __restrict__ state_idx, int P) {
     constexpr int VW = 16 * NVT;        // value columns per state wave
     constexpr int VB = NS * VW;         // value columns per workgroup
     constexpr int VSPLIT = D / VB;
@@ -497,6 +498,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
     };
     struct Item {
         int n, h, hq, vblock, seq_beg, seq_len, nch;
+        long slot;  // state of the sequence: state n or a pool slot
     };
     auto decode = [&](int item) -> Item {
         Item it;
@@ -510,6 +512,11 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
         it.seq_len = cu[it.n + 1] - it.seq_beg;
         // sequences of at most kRecurMax tokens belong to the recurrent kernel
         it.nch = it.seq_len <= kRecurMax ? 0 : (it.seq_len + C - 1) / C;
+        it.slot = it.n;
+        if (state_idx != nullptr) {
+            it.slot = state_idx[it.n];
+            if (it.slot < 0 || it.slot >= P) it.nch = 0;  // outside the pool: skipped
+        }
         return it;
     };
     const size_t qk_stride = (size_t)H_qk * D;
@@ -518,7 +525,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
     // Every wave stages chunk 0 of the first non-empty item (chunk 0 of the
     // stream) before the roles split, so the state waves can start on it while
     // producer 0 prepares the rest.
-    Item first = {0, 0, 0, 0, 0, 0, 0};
+    Item first = {0, 0, 0, 0, 0, 0, 0, 0};
     for (int pass = 0;; ++pass) {
         const int item = item_at(pass);
         if (item < 0) break;
@@ -561,7 +568,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
         const Item it = decode(item);
         if (it.nch == 0) continue;  // a short sequence: the recurrent kernel's
         const int h = it.h, seq_beg = it.seq_beg, seq_len = it.seq_len, nch = it.nch;
-        const size_t state_off = ((size_t)it.n * H_v + h) * D * D;
+        const size_t state_off = ((size_t)it.slot * H_v + h) * D * D;
         const int vcol0 = (it.vblock * NS + wave) * VW;
         f32x4_t st[NDT][NVT];  // st[dt][vt][i] = S[v][d], v = vcol0 + 16 vt + m, d = 16 dt + 4 gq + i
 #pragma unroll
@@ -966,7 +973,7 @@ static hipError_t launch_pipe(const PrefillArgs& a, const int32_t* order, hipStr
     hipLaunchKernelGGL((pipe::prefill_pipe_kernel<NS, NVT, NO>), dim3((unsigned)grid),
                        dim3(64 * (NS + NO + pipe::NP)), 0, stream, (const uint16_t*)a.q, (const uint16_t*)a.k,
                        (const uint16_t*)a.v, a.g, a.beta, a.cu_seqlens, order, a.initial_state, a.final_state,
-                       (uint16_t*)a.o, a.N, a.H_qk, a.H_v, a.scale);
+                       (uint16_t*)a.o, a.N, a.H_qk, a.H_v, a.scale, a.state_idx, a.P);
     return hipGetLastError();
 }
 

@@ -59,7 +59,8 @@ __global__ __launch_bounds__(256) void prefill_recur_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const float* __restrict__ g, const float* __restrict__ beta, const int32_t* __restrict__ cu,
     int32_t* __restrict__ order, const float* initial_state, float* final_state,
-    uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale) {
+    uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale,
+    const int32_t* __restrict__ state_idx, int P) {
     __shared__ Smem sm;
     __shared__ int nlong;
     if (blockIdx.x == 0) {
@@ -90,9 +91,17 @@ __global__ __launch_bounds__(256) void prefill_recur_kernel(
         const int t0 = cu[n];
         const int len = cu[n + 1] - t0;
         if (len > kRecurMax) continue;  // the chunk kernel's
+        // the state of sequence n: state n, or pool slot state_idx[n] (outside
+        // the pool: the sequence is skipped)
+        long shead = head;
+        if (state_idx != nullptr) {
+            const long slot = state_idx[n];
+            if (slot < 0 || slot >= P) continue;
+            shead = slot * H_v + h;
+        }
         const int row0 = blk * ROWS;
         const int row = row0 + wave * ROWS_PER_WAVE + sub;
-        const size_t srow = ((size_t)head * D + row) * D;
+        const size_t srow = ((size_t)shead * D + row) * D;
         f32x4_t s[J];
 #pragma unroll
         for (int j = 0; j < J; ++j) {
@@ -185,7 +194,7 @@ hipError_t launch_prefill_recur(const PrefillArgs& a, int32_t* order, hipStream_
     hipLaunchKernelGGL(recur::prefill_recur_kernel, dim3((unsigned)grid), dim3(64 * recur::NWAVE), 0, stream,
                        (const uint16_t*)a.q, (const uint16_t*)a.k, (const uint16_t*)a.v, a.g, a.beta,
                        a.cu_seqlens, order, a.initial_state, a.final_state, (uint16_t*)a.o, a.N, a.H_qk,
-                       a.H_v, a.scale);
+                       a.H_v, a.scale, a.state_idx, a.P);
     return hipGetLastError();
 }
 

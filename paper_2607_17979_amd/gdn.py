@@ -23,11 +23,12 @@ __all__ = [
     "gdn_decode_indexed",
     "gdn_prefill_workspace_size",
     "gdn_prefill_varlen",
+    "gdn_prefill_varlen_indexed",
     "EXPORTED_SYMBOLS",
 ]
 
 EXPORTED_SYMBOLS = ("gdn_last_error", "gdn_abi_version", "gdn_decode", "gdn_decode_indexed",
-                    "gdn_prefill_workspace_size", "gdn_prefill_varlen")
+                    "gdn_prefill_workspace_size", "gdn_prefill_varlen", "gdn_prefill_varlen_indexed")
 
 _STATUS = {0: "GDN_OK", -1: "GDN_EINVAL", -2: "GDN_EUNSUPPORTED", -3: "GDN_EALIGN",
            -4: "GDN_EWORKSPACE", -5: "GDN_EHIP"}
@@ -68,6 +69,9 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.gdn_prefill_varlen.restype = ci
     lib.gdn_prefill_varlen.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                        ci, ci, ci, ci, ci, ci, ci, cf, vp, sz, vp]
+    lib.gdn_prefill_varlen_indexed.restype = ci
+    lib.gdn_prefill_varlen_indexed.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                               ci, ci, ci, ci, ci, ci, ci, ci, cf, vp, sz, vp]
     if path is None:
         _lib = lib
     return lib
@@ -210,3 +214,40 @@ def gdn_prefill_varlen(q, k, v, g, beta, cu_seqlens, initial_state, final_state,
                                   _ptr(o), N, T, H_qk, H_v, D, D, chunk, float(scale),
                                   _ptr(workspace), workspace.numel() * workspace.element_size(),
                                   _stream(q, stream)))
+
+
+def gdn_prefill_varlen_indexed(q, k, v, g, beta, cu_seqlens, state_pool, state_idx, o,
+                               scale: float = 1.0, chunk: Optional[int] = None, workspace=None,
+                               stream=None) -> None:
+    """Packed varlen prefill on pooled states (see include/gdn.h).  As
+    gdn_prefill_varlen, with state_pool: fp32 [P, H_v, D, D] (sequence n starts
+    from slot state_idx[n] and leaves its final state there) and state_idx:
+    int32 [N] on the device (entries outside [0, P) skip the sequence)."""
+    import torch
+
+    T, H_qk, D = q.shape
+    H_v = v.shape[1]
+    N = cu_seqlens.shape[0] - 1
+    P = state_pool.shape[0]
+    dev = q.device
+    if dev.type != "cuda":
+        raise ValueError("tensors must be on a GPU device")
+    _need(q, "q", torch.bfloat16, (T, H_qk, D), dev)
+    _need(k, "k", torch.bfloat16, (T, H_qk, D), dev)
+    _need(v, "v", torch.bfloat16, (T, H_v, D), dev)
+    _need(g, "g", torch.float32, (T, H_v), dev)
+    _need(beta, "beta", torch.float32, (T, H_v), dev)
+    _need(cu_seqlens, "cu_seqlens", torch.int32, (N + 1,), dev)
+    _need(state_pool, "state_pool", torch.float32, (P, H_v, D, D), dev)
+    _need(state_idx, "state_idx", torch.int32, (N,), dev)
+    _need(o, "o", torch.bfloat16, (T, H_v, D), dev)
+    chunk = default_chunk(D) if chunk is None else chunk
+    need = gdn_prefill_workspace_size(N, T, H_qk, H_v, D, D, chunk)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    lib = load_library()
+    _check(lib.gdn_prefill_varlen_indexed(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
+                                          _ptr(cu_seqlens), _ptr(state_pool), _ptr(state_idx),
+                                          _ptr(o), N, T, P, H_qk, H_v, D, D, chunk, float(scale),
+                                          _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                          _stream(q, stream)))

@@ -164,3 +164,34 @@ def test_error_message_is_per_call(lib):
 def test_binding_raises_on_missing_library(tmp_path):
     with pytest.raises(RuntimeError, match="missing"):
         gdn.load_library(str(tmp_path / "nope.so"))
+
+
+def prefill_indexed(lib, q=P, k=P, v=P, g=P, beta=P, cu=P, pool=P, idx=P, o=P, N=3, T=10, Pn=4,
+                    H_qk=1, H_v=2, Dk=128, Dv=128, chunk=64, ws=P, ws_bytes=256):
+    return lib.gdn_prefill_varlen_indexed(q, k, v, g, beta, cu, pool, idx, o, N, T, Pn, H_qk, H_v, Dk,
+                                          Dv, chunk, 1.0, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(N=-1), EINVAL, "must be >= 0"),
+    (dict(Pn=-1), EINVAL, "P must be"),
+    (dict(H_qk=2, H_v=3), EINVAL, "multiple"),
+    (dict(chunk=32), EUNSUP, "chunk 32"),
+    (dict(cu=None), EINVAL, "cu_seqlens is NULL"),
+    (dict(pool=None), EINVAL, "state_pool is NULL"),
+    (dict(pool=P + 8), EALIGN, "state_pool"),
+    (dict(idx=None), EINVAL, "state_idx is NULL"),
+    (dict(idx=P + 1), EALIGN, "state_idx"),
+    (dict(Pn=1 << 30), EINVAL, "P * H_v"),
+    (dict(q=None), EINVAL, "q is NULL"),
+    (dict(ws=None), EWS, "workspace"),
+])
+def test_prefill_indexed_rejects(lib, kw, status, msg):
+    assert prefill_indexed(lib, **kw) == status
+    assert msg in gdn.gdn_last_error()
+
+
+def test_prefill_indexed_empty_is_noop(lib):
+    assert prefill_indexed(lib, q=None, k=None, v=None, g=None, beta=None, cu=None, pool=None, idx=None,
+                           o=None, N=0, T=0, ws=None, ws_bytes=0) == OK
+    assert prefill_indexed(lib, pool=None, idx=None, Pn=0) == OK

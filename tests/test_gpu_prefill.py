@@ -325,3 +325,51 @@ def test_decode_multitoken_workload_parity():
     o, fin = _prefill_gpu(inp, dev, in_place=True)
     units = [(n, (3 * n + 5) % w["H_v"]) for n in range(w["N"])] + [(0, h) for h in range(w["H_v"])]
     _sampled_check(inp, o, fin, units, "multi-token decode 64 x 4")
+
+
+
+@pytest.mark.parametrize("D", [16, 128])
+def test_prefill_indexed_pool(D):
+    """Sequences start from, and leave their final state in, the pool slots
+    state_idx names: slots and outputs equal gdn_prefill_varlen on the gathered
+    states bit for bit (both routes), and the oracle; other slots, and the
+    outputs of a sequence whose index is -1, are untouched."""
+    import torch
+
+    dev = device()
+    lengths = [0, 3, 8, 9, 70, 130] if D == 128 else [5, 0, 20, 33]
+    slots = np.array([7, -1, 2, 9, 0, 4] if D == 128 else [1, 3, -1, 0], np.int32)
+    P = 10 if D == 128 else 4
+    note(f"prefill indexed D={D} lengths {lengths} slots {slots.tolist()}")
+    inp = wl.prefill_inputs(49 + D, lengths, 2, 4, D)
+    rng = np.random.default_rng(50 + D)
+    pool_host = (0.02 * rng.standard_normal((P, 4, D, D))).astype(np.float32)
+    valid = (slots >= 0) & (slots < P)
+    q, k, v = (to_dev(x, dev, bf16=True) for x in (inp.q, inp.k, inp.v))
+    g, b, cu = to_dev(inp.g, dev), to_dev(inp.beta, dev), to_dev(inp.cu_seqlens, dev)
+    pool = to_dev(pool_host, dev)
+    o = torch.full((inp.q.shape[0], 4, D), float("nan"), dtype=torch.bfloat16, device=dev)
+    gdn.gdn_prefill_varlen_indexed(q, k, v, g, b, cu, pool, to_dev(slots, dev), o)
+    # the same sequences with gdn_prefill_varlen on the gathered states
+    init_host = np.stack([pool_host[s] if ok else np.zeros_like(pool_host[0]) for s, ok in zip(slots, valid)])
+    init = to_dev(init_host, dev)
+    fin = torch.empty_like(init)
+    o2 = torch.empty_like(o)
+    gdn.gdn_prefill_varlen(q, k, v, g, b, cu, init, fin, o2)
+    torch.cuda.synchronize()
+    cu_h = inp.cu_seqlens
+    pool_np, fin_np = pool.cpu().numpy(), fin.cpu().numpy()
+    for n, (s, ok) in enumerate(zip(slots, valid)):
+        rows = slice(cu_h[n], cu_h[n + 1])
+        if ok:
+            assert np.array_equal(pool_np[s], fin_np[n]), n
+            assert torch.equal(o[rows].view(torch.int16), o2[rows].view(torch.int16)), n
+        else:
+            assert torch.isnan(o[rows].float()).all(), n
+    untouched = np.setdiff1d(np.arange(P), slots[valid])
+    assert np.array_equal(pool_np[untouched], pool_host[untouched])
+    o_ref, s_ref = ref.prefill_varlen(inp.q, inp.k, inp.v, inp.g, inp.beta, cu_h, init_host,
+                                      scale=inp.scale)
+    keep = np.concatenate([np.arange(cu_h[n], cu_h[n + 1]) for n in range(len(lengths)) if valid[n]])
+    check_outputs(bf16_np(o)[keep], o_ref[keep], f"indexed D={D}")
+    check_states(pool_np[slots[valid]], s_ref[valid], f"indexed D={D}")
