@@ -82,35 +82,65 @@ __global__ __launch_bounds__(256) void prefill_recur_kernel(
     const int sub = lane / LPR, c = lane % LPR;
     const long units = (long)N * H_v * BPH;
     const size_t qk_stride = (size_t)H_qk * D, v_stride = (size_t)H_v * D;
-    for (long u = blockIdx.x - 1; u < units; u += gridDim.x - 1) {
-        const long head = u / BPH;  // n H_v + h
-        const int blk = (int)(u - head * BPH);
-        const int n = (int)(head / H_v);
-        const int h = (int)(head - (long)n * H_v);
-        const int hq = h / (H_v / H_qk);
-        const int t0 = cu[n];
-        const int len = cu[n + 1] - t0;
-        if (len > kRecurMax) continue;  // the chunk kernel's
-        // the state of sequence n: state n, or pool slot state_idx[n] (outside
-        // the pool: the sequence is skipped)
-        long shead = head;
+    // Unit u runs here if its sequence has at most kRecurMax tokens and its
+    // state lies inside the pool; a workgroup walks units u, u + stride, ...
+    const long stride = gridDim.x - 1;
+    auto runs_here = [&](long u) -> bool {
+        const int n = (int)(u / BPH / H_v);
+        if (cu[n + 1] - cu[n] > kRecurMax) return false;  // the chunk kernel's
         if (state_idx != nullptr) {
-            const long slot = state_idx[n];
-            if (slot < 0 || slot >= P) continue;
-            shead = slot * H_v + h;
+            const int slot = state_idx[n];
+            if (slot < 0 || slot >= P) return false;  // outside the pool: skipped
         }
-        const int row0 = blk * ROWS;
-        const int row = row0 + wave * ROWS_PER_WAVE + sub;
-        const size_t srow = ((size_t)shead * D + row) * D;
-        f32x4_t s[J];
+        return true;
+    };
+    auto next_unit = [&](long u) -> long {
+        while (u < units && !runs_here(u)) u += stride;
+        return u;
+    };
+    // The fields of a unit that runs here: its state (state n, or pool slot
+    // state_idx[n]), head, row block and tokens.
+    struct Unit {
+        long u, shead;
+        int h, hq, blk, t0, len;
+    };
+    auto unit_at = [&](long u) -> Unit {
+        Unit r;
+        const long head = u / BPH;  // n H_v + h
+        const int n = (int)(head / H_v);
+        r.u = u;
+        r.h = (int)(head - (long)n * H_v);
+        r.hq = r.h / (H_v / H_qk);
+        r.blk = (int)(u - head * BPH);
+        r.t0 = cu[n];
+        r.len = cu[n + 1] - r.t0;
+        r.shead = state_idx != nullptr ? (long)state_idx[n] * H_v + r.h : head;
+        return r;
+    };
+    auto state_row = [&](const Unit& x) {
+        const int row = x.blk * ROWS + wave * ROWS_PER_WAVE + sub;
+        return ((size_t)x.shead * D + row) * D;
+    };
+    auto load_rows = [&](const Unit& x, f32x4_t (&r)[J]) {
+        const size_t srow = state_row(x);
 #pragma unroll
         for (int j = 0; j < J; ++j) {
             if (initial_state != nullptr)
-                s[j] = __builtin_nontemporal_load(
+                r[j] = __builtin_nontemporal_load(
                     reinterpret_cast<const f32x4_t*>(initial_state + srow + (j * LPR + c) * 4));
             else
-                s[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+                r[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
         }
+    };
+    long ucur = next_unit(blockIdx.x - 1);
+    f32x4_t s[J];
+    if (ucur < units) load_rows(unit_at(ucur), s);
+    while (ucur < units) {
+        const Unit cur = unit_at(ucur);
+        const long unxt = next_unit(ucur + stride);
+        const int h = cur.h, hq = cur.hq, t0 = cur.t0, len = cur.len;
+        const int row0 = cur.blk * ROWS;
+        const int row = row0 + wave * ROWS_PER_WAVE + sub;
         // stage the tokens: 16 segments of 8 values per k or q row, 4 per v slice
         if (tid < len * (D / 8)) {
             const int t = tid / (D / 8), seg = tid - t * (D / 8);
@@ -151,6 +181,10 @@ __global__ __launch_bounds__(256) void prefill_recur_kernel(
             if (c == 0) sm.tok.kq[t] = kq;
         }
         __syncthreads();
+        // the next unit's state rows, in flight during this unit's token loop
+        // (issued after the staging loads, which the counters retire in order)
+        f32x4_t sn[J];
+        if (unxt < units) load_rows(unit_at(unxt), sn);
         for (int t = 0; t < len; ++t) {
             f32x4_t kf[J], qf[J];
 #pragma unroll
@@ -177,9 +211,15 @@ __global__ __launch_bounds__(256) void prefill_recur_kernel(
             if (c == 0)
                 o[(size_t)(t0 + t) * v_stride + (size_t)h * D + row] = f32_to_bf16(scale * fmaf(alpha, sq, uu * kq));
         }
+        const size_t srow = state_row(cur);
 #pragma unroll
         for (int j = 0; j < J; ++j)
             __builtin_nontemporal_store(s[j], reinterpret_cast<f32x4_t*>(final_state + srow + (j * LPR + c) * 4));
+        if (unxt < units) {
+#pragma unroll
+            for (int j = 0; j < J; ++j) s[j] = sn[j];
+        }
+        ucur = unxt;
         __syncthreads();  // the staged tokens are read; the next unit may overwrite them
     }
 }

@@ -373,3 +373,46 @@ def test_prefill_indexed_pool(D):
     keep = np.concatenate([np.arange(cu_h[n], cu_h[n + 1]) for n in range(len(lengths)) if valid[n]])
     check_outputs(bf16_np(o)[keep], o_ref[keep], f"indexed D={D}")
     check_states(pool_np[slots[valid]], s_ref[valid], f"indexed D={D}")
+
+
+def test_prefill_indexed_pool_many_short_sequences():
+    """800 sequences of 0..8 tokens on a 1,000-slot pool (shuffled slots, some
+    -1): every token-by-token workgroup walks several units, prefetching the
+    next unit's state.  Slots and outputs equal gdn_prefill_varlen on the
+    gathered states bit for bit; skipped sequences' rows and unnamed slots are
+    untouched; the oracle on every sequence."""
+    import torch
+
+    dev = device()
+    rng = np.random.default_rng(52)
+    N, P, D = 800, 1000, 128
+    lengths = rng.integers(0, 9, size=N).tolist()
+    slots = rng.permutation(P)[:N].astype(np.int32)
+    slots[rng.choice(N, size=40, replace=False)] = -1
+    valid = slots >= 0
+    note(f"prefill indexed, {N} short sequences, T={sum(lengths)}")
+    inp = wl.prefill_inputs(53, lengths, 2, 4, D)
+    pool_host = (0.02 * rng.standard_normal((P, 4, D, D))).astype(np.float32)
+    q, k, v = (to_dev(x, dev, bf16=True) for x in (inp.q, inp.k, inp.v))
+    g, b, cu = to_dev(inp.g, dev), to_dev(inp.beta, dev), to_dev(inp.cu_seqlens, dev)
+    pool = to_dev(pool_host, dev)
+    o = torch.full((inp.q.shape[0], 4, D), float("nan"), dtype=torch.bfloat16, device=dev)
+    gdn.gdn_prefill_varlen_indexed(q, k, v, g, b, cu, pool, to_dev(slots, dev), o)
+    init_host = np.where(valid[:, None, None, None], pool_host[np.maximum(slots, 0)], 0.0).astype(np.float32)
+    init = to_dev(init_host, dev)
+    fin = torch.empty_like(init)
+    o2 = torch.empty_like(o)
+    gdn.gdn_prefill_varlen(q, k, v, g, b, cu, init, fin, o2)
+    torch.cuda.synchronize()
+    pool_np, fin_np = pool.cpu().numpy(), fin.cpu().numpy()
+    assert np.array_equal(pool_np[slots[valid]], fin_np[valid])
+    cu_h = inp.cu_seqlens
+    keep = np.concatenate([np.arange(cu_h[n], cu_h[n + 1]) for n in range(N) if valid[n]])
+    skip = np.concatenate([np.arange(cu_h[n], cu_h[n + 1]) for n in range(N) if not valid[n]])
+    assert torch.equal(o[keep].view(torch.int16), o2[keep].view(torch.int16))
+    assert torch.isnan(o[skip].float()).all()
+    untouched = np.setdiff1d(np.arange(P), slots[valid])
+    assert np.array_equal(pool_np[untouched], pool_host[untouched])
+    o_ref, s_ref = ref.prefill_varlen(inp.q, inp.k, inp.v, inp.g, inp.beta, cu_h, init_host, scale=inp.scale)
+    check_outputs(bf16_np(o)[keep], o_ref[keep], "indexed, many short")
+    check_states(pool_np[slots[valid]], s_ref[valid], "indexed, many short")
