@@ -54,12 +54,22 @@ constexpr int NBLK = NCT * (NCT + 1) / 2;   // lower-triangular 16 x 16 blocks (
 constexpr int SEGS = D / 8;                 // 16-byte segments per q/k/v row
 constexpr int SITEMS = C * SEGS / 64;       // staged segments per producer lane (16)
 constexpr int SP = 20;                      // row pitch (fp32) of the producers' 16 x 16 scratch blocks
+// Block pitch (fp32) of that scratch: 4 words of padding, so that the four
+// lane groups, each reading a row of its own block, hit different banks.
+constexpr int SBS = 16 * SP + 4;
 constexpr int kSpinLimit = 1 << 20;
 
 __device__ __forceinline__ constexpr int bidx(int i, int j) { return i * (i + 1) / 2 + j; }
 
+// Column of the 4-element unit u of row r in a stored 16 x 16 bf16 block: the
+// units of a row rotate with r / 4.  The 8-byte stores of one unit column
+// (16 lanes, rows 0..15) then cover all 128 bytes of banks a store cycle
+// serves, and the 8-byte reads of 32 lanes all 256 bytes of a read cycle.
+__device__ __forceinline__ int bsw(int r, int u) { return 4 * (u ^ ((r >> 2) & 3)); }
+
 // Results of the state-independent part of one chunk.
 struct Slot {
+    // 16 x 16 blocks, the 4-element units of each row placed by bsw
     uint16_t th[NBLK][16][16];   // T diag(beta) by lower blocks, transposed [col][row], bf16 hi
     uint16_t tl[NBLK][16][16];   // bf16 lo
     uint16_t pm[NBLK][16][16];   // scale (M o Q K^T) by lower blocks [row t][col s], bf16
@@ -88,7 +98,7 @@ struct Smem {
     uint16_t qb[C][PD];               // Q rows of the chunk in flight
     uint16_t vb[C][VB + 16];          // V rows, the workgroup's columns (swizzled, see PD)
     Slot slot[NP];
-    alignas(16) float scr[NP][NCT * 16 * SP];  // per producer: diagonal blocks of A, then of T
+    alignas(16) float scr[NP][NCT * SBS];  // per producer: diagonal blocks of A, then of T
     alignas(16) float gam[NP][C];     // per producer: gate prefix of its chunk
     alignas(16) float bet[NP][C];     // per producer: beta of its chunk
     uint16_t zero[16][16];            // stands in for blocks above the diagonal
@@ -130,17 +140,29 @@ __device__ __forceinline__ void wait_ge(unsigned* ctr, unsigned target) {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
+typedef unsigned u32x2_t __attribute__((ext_vector_type(2)));
+
+// An 8-byte LDS read that stays a ds_read_b64 of its own.  Two 8-byte reads
+// off one base would otherwise become one ds_read2_b64, which serves 16 lanes
+// per cycle and word over 128 bytes of banks; a ds_read_b64 serves 32 lanes
+// per cycle over 256 bytes, so the pair costs 4 LDS cycles instead of 8, and
+// the operand patterns here, laid out for 256 bytes, stay conflict-free.
+// (The volatile access is what keeps the compiler from pairing the two.)
+__device__ __forceinline__ u32x2_t lds_ld8_alone(const uint16_t* p) {
+    return *(const volatile __attribute__((address_space(3))) u32x2_t*)p;
+}
+
 // A (or B) operand from a stored lower-triangular block matrix (block row ct,
 // contraction columns kc..kc+31 in the permuted order); blocks above the
 // diagonal read the zero block.
 __device__ __forceinline__ bf16x8_t blk_frag(const uint16_t (*blocks)[16][16], const uint16_t (*zero)[16],
                                              int ct, int kc, int m, int g) {
     const int j0 = kc >> 4;
-    const uint16_t* p0 = &blocks[bidx(ct, j0)][m][swz(m, 4 * g)];
-    const uint16_t* p1 = (j0 + 1 <= ct) ? &blocks[bidx(ct, j0 + 1)][m][swz(m, 4 * g)] : &zero[m][4 * g];
-    const uint2 lo = *reinterpret_cast<const uint2*>(p0);
-    const uint2 hi = *reinterpret_cast<const uint2*>(p1);
-    uint4 u = {lo.x, lo.y, hi.x, hi.y};
+    const uint16_t* p0 = &blocks[bidx(ct, j0)][m][bsw(m, g)];
+    const uint16_t* p1 = (j0 + 1 <= ct) ? &blocks[bidx(ct, j0 + 1)][m][bsw(m, g)] : &zero[m][bsw(m, g)];
+    const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(p0);
+    const u32x2_t hi = lds_ld8_alone(p1);
+    uint4 u = {lo[0], lo[1], hi[0], hi[1]};
     return __builtin_bit_cast(bf16x8_t, u);
 }
 
@@ -174,7 +196,7 @@ __device__ __forceinline__ bf16x8_t lds_frag_tr(const uint16_t (*a)[PD], int r0,
 __device__ __forceinline__ bf16x8_t blk_frag_t(const uint16_t (*blocks)[16][16], const uint16_t (*zero)[16],
                                                int ct, int kc, int m, int g) {
     const int j0 = kc >> 4;
-    const int r = 4 * g + (m >> 2), cc = 4 * (m & 3);
+    const int r = 4 * g + (m >> 2), cc = bsw(r, m & 3);
     const uint2 lo = lds_tr4(&blocks[bidx(ct, j0)][r][cc]);
     const uint2 hi = lds_tr4((j0 + 1 <= ct) ? &blocks[bidx(ct, j0 + 1)][r][cc] : &zero[r][cc]);
     uint4 u = {lo.x, lo.y, hi.x, hi.y};
@@ -214,8 +236,8 @@ __device__ __forceinline__ void store_split_t(uint16_t (*th)[16], uint16_t (*tl)
     uint2 hi, lo;
     split_pair(x[0] * scale, x[1] * scale, hi.x, lo.x);
     split_pair(x[2] * scale, x[3] * scale, hi.y, lo.y);
-    *reinterpret_cast<uint2*>(&th[m][4 * g]) = hi;
-    *reinterpret_cast<uint2*>(&tl[m][4 * g]) = lo;
+    *reinterpret_cast<uint2*>(&th[m][bsw(m, g)]) = hi;
+    *reinterpret_cast<uint2*>(&tl[m][bsw(m, g)]) = lo;
 }
 
 // Context of a producer wave: values fixed for the whole sequence.
@@ -236,9 +258,9 @@ struct ProdCtx {
 // tiles (slot j < 4: column k0 + 4 g + j, slot j >= 4: k0 + 16 + 4 g + j - 4).
 __device__ __forceinline__ bf16x8_t row_frag(const uint16_t (*a)[PD], int r, int k0, int g) {
     const int cl = swz(r, 4 * g);
-    const uint2 lo = *reinterpret_cast<const uint2*>(&a[r][k0 + cl]);
-    const uint2 hi = *reinterpret_cast<const uint2*>(&a[r][k0 + 16 + cl]);
-    uint4 u = {lo.x, lo.y, hi.x, hi.y};
+    const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(&a[r][k0 + cl]);
+    const u32x2_t hi = lds_ld8_alone(&a[r][k0 + 16 + cl]);
+    uint4 u = {lo[0], lo[1], hi[0], hi[1]};
     return __builtin_bit_cast(bf16x8_t, u);
 }
 
@@ -344,10 +366,10 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
     //      block b (rows of N_b are read as LDS broadcasts); then block
     //      columns T_bJ = -D_b sum_{kb=J}^{b-1} A_{b,kb} T_{kb,J} (b > J)
     //      on split-bf16 MFMA.
-    float* scb = scr + gq * 16 * SP;  // this lane's block b = gq
+    float* scb = scr + gq * SBS;  // this lane's block b = gq
 #pragma unroll
     for (int b = 0; b < NCT; ++b)     // row m of N_b, columns 4 gq .. 4 gq + 3
-        *reinterpret_cast<f32x4_t*>(&scr[(16 * b + m) * SP + 4 * gq]) = nt[b];
+        *reinterpret_cast<f32x4_t*>(&scr[b * SBS + m * SP + 4 * gq]) = nt[b];
     // Row r + 1 of N_b is read while row r is solved; the scheduling
     // fences keep the reads from being hoisted all at once.
     float xs[16];
@@ -374,10 +396,10 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
     f32x4_t dd[NCT], ddt[NCT], tt[NBLK];
 #pragma unroll
     for (int b = 0; b < NCT; ++b) {     // acc(D_b): D_b[4 gq + i][m]
-        dd[b] = *reinterpret_cast<const f32x4_t*>(&scr[(16 * b + m) * SP + 4 * gq]);
+        dd[b] = *reinterpret_cast<const f32x4_t*>(&scr[b * SBS + m * SP + 4 * gq]);
         if (b > 0) {                    // -acc(D_b^T): -D_b[m][4 gq + i]
 #pragma unroll
-            for (int i = 0; i < 4; ++i) ddt[b][i] = -scr[(16 * b + 4 * gq + i) * SP + m];
+            for (int i = 0; i < 4; ++i) ddt[b][i] = -scr[b * SBS + (4 * gq + i) * SP + m];
         }
     }
     {
@@ -410,7 +432,7 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
     for (int b = 0; b < NCT; ++b)
 #pragma unroll
         for (int jt = 0; jt <= b; ++jt)
-            *reinterpret_cast<uint2*>(&sl.pm[bidx(b, jt)][m][swz(m, 4 * gq)]) = pk[bidx(b, jt)];
+            *reinterpret_cast<uint2*>(&sl.pm[bidx(b, jt)][m][bsw(m, gq)]) = pk[bidx(b, jt)];
 #pragma unroll
     for (int b = 0; b < NCT; ++b) {
         store_split_t(sl.th[bidx(b, b)], sl.tl[bidx(b, b)], dd[b], br[b], m, gq);
@@ -441,8 +463,12 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
     // V rows of the workgroup's VB columns (VB / 8 lanes per row), loaded into
     // the registers the K rows held, so that their latency overlaps the wait
     // for the Q and V buffers
+    // With 4 lanes per row, rows 2i + 1 and 2i + 2 swap their lanes, so that
+    // each 8 lanes (one store cycle) write two rows 192 bytes apart, which
+    // share no banks.
     constexpr int VLR = VB / 8, VRI = 64 / VLR, VIT = C / VRI;
-    const int vr = lane / VLR, vsg = lane - vr * VLR;
+    const int vq = lane / VLR, vsg = lane - vq * VLR;
+    const int vr = VLR == 4 ? (vq & ~3) | ((vq & 1) << 1) | ((vq >> 1) & 1) : vq;
     const uint16_t* vc0 = pc.v + (size_t)tb * pc.v_stride + (size_t)pc.h * D + pc.vcb0;
     uint4 sv[VIT];
 #pragma unroll
