@@ -140,6 +140,19 @@ __device__ __forceinline__ void wait_ge(unsigned* ctr, unsigned target) {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
+// A counter's value now, for a later wait_seen: the LDS round trip of the
+// read overlaps the work in between.
+__device__ __forceinline__ unsigned peek(unsigned* ctr) {
+    return __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// wait_ge for a counter read earlier as `seen`: counters only grow, so a seen
+// value at the target needs no further read.
+__device__ __forceinline__ void wait_seen(unsigned* ctr, unsigned target, unsigned seen) {
+    if (__builtin_amdgcn_readfirstlane(seen) < target) wait_ge(ctr, target);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 typedef unsigned u32x2_t __attribute__((ext_vector_type(2)));
 
 // An 8-byte LDS read that stays a ds_read_b64 of its own.  Two 8-byte reads
@@ -616,9 +629,21 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
             const int t0 = seq_beg + c * C;
             const Slot& sl = sm.slot[xs % NP];
             const uint16_t (*kb)[PD] = sm.kb[par];
-            wait_ge(&sm.cnt[CNT_STG], (unsigned)(xs + 1));
-            // with output waves: the previous chunk's S0 hi operands were read
-            if constexpr (NO > 0) wait_ge(&sm.cnt[CNT_HAND0 + 4 * wave + 1], (unsigned)xs);
+            // With output waves (where these waits are mostly met on arrival)
+            // every counter the chunk waits for is read here at once, and a
+            // wait reads again only if its value was short.
+            unsigned seen_hs = 0, seen_rdy = 0, seen_hu = 0;
+            if constexpr (NO > 0) {
+                const unsigned seen_stg = peek(&sm.cnt[CNT_STG]);
+                seen_hs = peek(&sm.cnt[CNT_HAND0 + 4 * wave + 1]);
+                seen_rdy = peek(&sm.cnt[CNT_READY0 + xs % NP]);
+                seen_hu = peek(&sm.cnt[CNT_HAND0 + 4 * wave + 3]);
+                wait_seen(&sm.cnt[CNT_STG], (unsigned)(xs + 1), seen_stg);
+                // the previous chunk's S0 hi operands were read
+                wait_seen(&sm.cnt[CNT_HAND0 + 4 * wave + 1], (unsigned)xs, seen_hs);
+            } else {
+                wait_ge(&sm.cnt[CNT_STG], (unsigned)(xs + 1));
+            }
             // K S0^T (S0 hi + lo), rows t; (Q S0^T)^T (S0 hi), rows v, unless
             // an output wave takes it (it gets the S0 hi operands instead)
             f32x4_t ks[NCT][NVT], ot[NVT][NCT];
@@ -675,7 +700,10 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
             }
             if constexpr (NO > 0) signal(&sm.cnt[CNT_HAND0 + 4 * wave + 0], lane);
             // W = V - diag(exp(gamma)) K S0^T (in ks)
-            wait_ge(&sm.cnt[CNT_READY0 + xs % NP], (unsigned)(xs / NP + 1));
+            if constexpr (NO > 0)
+                wait_seen(&sm.cnt[CNT_READY0 + xs % NP], (unsigned)(xs / NP + 1), seen_rdy);
+            else
+                wait_ge(&sm.cnt[CNT_READY0 + xs % NP], (unsigned)(xs / NP + 1));
             // T operands of U = T diag(beta) W, read now so that their latency
             // hides behind the vector work of W
             bf16x8_t tah[NCT][2], tal[NCT][2];
@@ -740,7 +768,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
             }
             if constexpr (NO > 0) {
                 // the previous chunk's U hi operands were read
-                wait_ge(&sm.cnt[CNT_HAND0 + 4 * wave + 3], (unsigned)xs);
+                wait_seen(&sm.cnt[CNT_HAND0 + 4 * wave + 3], (unsigned)xs, seen_hu);
 #pragma unroll
                 for (int kc = 0; kc < C; kc += 32)
 #pragma unroll
