@@ -601,6 +601,10 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
         // ======================= state waves ===================================
         const SplitMasks spm = split_masks();
         int xs = 0;  // stream index of the next chunk
+        // The counters chunk xs waits for, read at the end of chunk xs - 1
+        // (their LDS round trip overlaps that chunk's output stores); a wait
+        // reads again only if the value seen was short.  0: nothing seen yet.
+        unsigned seen_stg = 0, seen_hs = 0, seen_rdy = 0, seen_hu = 0;
         for (int pass = 0;; ++pass) {
         const int item = item_at(pass);
         if (item < 0) break;
@@ -629,21 +633,12 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
             const int t0 = seq_beg + c * C;
             const Slot& sl = sm.slot[xs % NP];
             const uint16_t (*kb)[PD] = sm.kb[par];
-            // With output waves (where these waits are mostly met on arrival)
-            // every counter the chunk waits for is read here at once, and a
-            // wait reads again only if its value was short.
-            unsigned seen_hs = 0, seen_rdy = 0, seen_hu = 0;
-            if constexpr (NO > 0) {
-                const unsigned seen_stg = peek(&sm.cnt[CNT_STG]);
-                seen_hs = peek(&sm.cnt[CNT_HAND0 + 4 * wave + 1]);
-                seen_rdy = peek(&sm.cnt[CNT_READY0 + xs % NP]);
-                seen_hu = peek(&sm.cnt[CNT_HAND0 + 4 * wave + 3]);
-                wait_seen(&sm.cnt[CNT_STG], (unsigned)(xs + 1), seen_stg);
-                // the previous chunk's S0 hi operands were read
-                wait_seen(&sm.cnt[CNT_HAND0 + 4 * wave + 1], (unsigned)xs, seen_hs);
-            } else {
-                wait_ge(&sm.cnt[CNT_STG], (unsigned)(xs + 1));
-            }
+            // (uniform values, held in scalar registers through the chunk)
+            const unsigned rdy_seen = __builtin_amdgcn_readfirstlane(seen_rdy);
+            const unsigned hu_seen = __builtin_amdgcn_readfirstlane(seen_hu);
+            wait_seen(&sm.cnt[CNT_STG], (unsigned)(xs + 1), seen_stg);
+            // with output waves: the previous chunk's S0 hi operands were read
+            if constexpr (NO > 0) wait_seen(&sm.cnt[CNT_HAND0 + 4 * wave + 1], (unsigned)xs, seen_hs);
             // K S0^T (S0 hi + lo), rows t; (Q S0^T)^T (S0 hi), rows v, unless
             // an output wave takes it (it gets the S0 hi operands instead)
             f32x4_t ks[NCT][NVT], ot[NVT][NCT];
@@ -700,10 +695,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
             }
             if constexpr (NO > 0) signal(&sm.cnt[CNT_HAND0 + 4 * wave + 0], lane);
             // W = V - diag(exp(gamma)) K S0^T (in ks)
-            if constexpr (NO > 0)
-                wait_seen(&sm.cnt[CNT_READY0 + xs % NP], (unsigned)(xs / NP + 1), seen_rdy);
-            else
-                wait_ge(&sm.cnt[CNT_READY0 + xs % NP], (unsigned)(xs / NP + 1));
+            wait_seen(&sm.cnt[CNT_READY0 + xs % NP], (unsigned)(xs / NP + 1), rdy_seen);
             // T operands of U = T diag(beta) W, read now so that their latency
             // hides behind the vector work of W
             bf16x8_t tah[NCT][2], tal[NCT][2];
@@ -768,7 +760,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
             }
             if constexpr (NO > 0) {
                 // the previous chunk's U hi operands were read
-                wait_seen(&sm.cnt[CNT_HAND0 + 4 * wave + 3], (unsigned)xs, seen_hu);
+                wait_seen(&sm.cnt[CNT_HAND0 + 4 * wave + 3], (unsigned)xs, hu_seen);
 #pragma unroll
                 for (int kc = 0; kc < C; kc += 32)
 #pragma unroll
@@ -840,6 +832,12 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
             }
             // all LDS reads of chunk c are done: its K buffer and result slot are free
             signal(&sm.cnt[CNT_DONE], lane);
+            seen_stg = peek(&sm.cnt[CNT_STG]);
+            seen_rdy = peek(&sm.cnt[CNT_READY0 + (xs + 1) % NP]);
+            if constexpr (NO > 0) {
+                seen_hs = peek(&sm.cnt[CNT_HAND0 + 4 * wave + 1]);
+                seen_hu = peek(&sm.cnt[CNT_HAND0 + 4 * wave + 3]);
+            }
             if constexpr (NO == 0) {
                 // Outputs: lane m + 16 gq holds, in ot[vt][ct], token 16 ct + m and
                 // value columns 16 vt + 4 gq .. + 3.  Two such tiles x, y are merged
