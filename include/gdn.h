@@ -117,8 +117,9 @@ GDN_API int gdn_decode_indexed(const void* q, const void* k, const void* v,
 
 /*
  * Bytes of device workspace gdn_prefill_varlen needs for N sequences (the
- * longest-first schedule, one int32 per sequence, and one int32 count of the
- * sequences run in chunks; rounded up to 256 bytes).
+ * longest-first schedule, one int32 per sequence, one int32 count of the
+ * sequences run in chunks and one int32 wait-fault word; rounded up to 256
+ * bytes).
  * Returns 0 for invalid arguments.
  */
 GDN_API size_t gdn_prefill_workspace_size(int N, int T, int H_qk, int H_v,
@@ -146,7 +147,13 @@ GDN_API size_t gdn_prefill_workspace_size(int N, int T, int H_qk, int H_v,
  *   o              bf16 [T, H_v, D]
  *   workspace      device buffer of at least
  *                  gdn_prefill_workspace_size(...) bytes, 256-byte aligned;
- *                  its contents are scratch (overwritten by each call).
+ *                  its contents are scratch (overwritten by each call).  Once
+ *                  the call has completed on the stream, int32 word N + 1 of
+ *                  it is 0, or nonzero if a wave of the chunk kernel gave up
+ *                  one of its bounded waits for another wave (a broken
+ *                  synchronisation, never expected): the call's results are
+ *                  then invalid.  A diagnostic read, not a status the call
+ *                  returns (the call does not wait for its kernels).
  *
  * For D = 128, sequences of at most 8 tokens are computed token by token in
  * fp32 (the decode arithmetic), longer ones in chunks; the choice depends

@@ -49,14 +49,18 @@ hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream);
 constexpr int kRecurMax = 8;
 hipError_t launch_prefill_recur(const PrefillArgs& a, int32_t* order, hipStream_t stream);
 // d = 128, chunk 64: the pipelined kernel (gdn_prefill_pipe.hip); `order` is the
-// longest-first schedule already written to the workspace.
-hipError_t launch_prefill_pipe(const PrefillArgs& a, const int32_t* order, hipStream_t stream);
+// workspace, holding the longest-first schedule already written (the kernel
+// sets its wait-fault word).
+hipError_t launch_prefill_pipe(const PrefillArgs& a, int32_t* order, hipStream_t stream);
 // Compute units of the current device (queried once per device).
 int device_compute_units();
 
 // Workspace layout of the prefill: int32 order[N] (sequence indices sorted by
 // length, longest first, ties by index), then (d = 128) int32 order[N] = the
-// number of sequences longer than kRecurMax; rounded up to 256 bytes.
+// number of sequences longer than kRecurMax, then int32 order[N + 1] = the
+// wait-fault word (cleared by the call's first launch, set by any wave of the
+// chunk kernel whose counter wait ran out of its bound); rounded up to 256
+// bytes.
 size_t prefill_workspace_bytes(int N);
 
 }  // namespace gdn

@@ -87,6 +87,7 @@ struct Smem {
 __global__ __launch_bounds__(256) void prefill_schedule_kernel(const int32_t* __restrict__ cu,
                                                                int N, int32_t* __restrict__ order) {
     __shared__ int len[kSortMax];
+    if (threadIdx.x == 0) order[N + 1] = 0;  // no waits here: the fault word stays clear
     schedule_longest_first(cu, N, order, len);
 }
 
@@ -480,7 +481,7 @@ __global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
 
 size_t prefill_workspace_bytes(int N) {
     if (N <= 0) return 0;
-    return ((size_t)(N + 1) * sizeof(int32_t) + 255) / 256 * 256;
+    return ((size_t)(N + 2) * sizeof(int32_t) + 255) / 256 * 256;
 }
 
 hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {

@@ -131,12 +131,16 @@ __device__ __forceinline__ void signal(unsigned* ctr, int lane) {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
-// Wait until *ctr >= target (bounded: never spins forever).
-__device__ __forceinline__ void wait_ge(unsigned* ctr, unsigned target) {
-    for (int it = 0; it < kSpinLimit; ++it) {
+// Wait until *ctr >= target (bounded: never spins forever).  A wait that runs
+// out of its bound (a broken synchronisation, never expected) sets *fault, so
+// that the caller can tell that the call's results are invalid.
+__device__ __forceinline__ void wait_ge(unsigned* ctr, unsigned target, int* fault) {
+    int it = 0;
+    for (; it < kSpinLimit; ++it) {
         if (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) >= target) break;
         __builtin_amdgcn_s_sleep(1);
     }
+    if (it == kSpinLimit) __hip_atomic_fetch_or(fault, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
@@ -148,8 +152,8 @@ __device__ __forceinline__ unsigned peek(unsigned* ctr) {
 
 // wait_ge for a counter read earlier as `seen`: counters only grow, so a seen
 // value at the target needs no further read.
-__device__ __forceinline__ void wait_seen(unsigned* ctr, unsigned target, unsigned seen) {
-    if (__builtin_amdgcn_readfirstlane(seen) < target) wait_ge(ctr, target);
+__device__ __forceinline__ void wait_seen(unsigned* ctr, unsigned target, unsigned seen, int* fault) {
+    if (__builtin_amdgcn_readfirstlane(seen) < target) wait_ge(ctr, target, fault);
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
@@ -264,6 +268,7 @@ struct ProdCtx {
     int seq_beg, seq_len, hq, h, H_v, pw;
     int vcb0;   // first value column of the workgroup
     float scale;
+    int* fault; // set by a wait that runs out of its bound
 };
 
 // A/B operand from row r of a swizzled row buffer, contraction columns
@@ -440,7 +445,7 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
     }
     // ---- publish to the slot once the state waves are done with its
     //      previous chunk
-    wait_ge(&sm.cnt[CNT_DONE], (unsigned)(x >= 4 ? NSIG * (x - 3) : 0));   // chunk x - 4 done
+    wait_ge(&sm.cnt[CNT_DONE], (unsigned)(x >= 4 ? NSIG * (x - 3) : 0), pc.fault);   // chunk x - 4 done
 #pragma unroll
     for (int b = 0; b < NCT; ++b)
 #pragma unroll
@@ -470,7 +475,7 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
         sq[it] = ld16(qc0, 2u * off);
     }
     // K buffer x & 1 was last read by the update of chunk x - 2
-    wait_ge(&sm.cnt[CNT_DONE], (unsigned)(x >= 2 ? NSIG * (x - 1) : 0));
+    wait_ge(&sm.cnt[CNT_DONE], (unsigned)(x >= 2 ? NSIG * (x - 1) : 0), pc.fault);
 #pragma unroll
     for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.kb[x & 1][4 * it + gq][swz(4 * it + gq, m * 8)]) = sk[it];
     // V rows of the workgroup's VB columns (VB / 8 lanes per row), loaded into
@@ -489,7 +494,7 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
         sv[it] = uint4{0, 0, 0, 0};
         sv[it] = ld16(vc0, 2u * ((unsigned)min(VRI * it + vr, L - 1) * (unsigned)pc.v_stride + 8u * vsg));
     }
-    wait_ge(&sm.cnt[CNT_QVFREE], (unsigned)(NSIG * x));
+    wait_ge(&sm.cnt[CNT_QVFREE], (unsigned)(NSIG * x), pc.fault);
 #pragma unroll
     for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.qb[4 * it + gq][swz(4 * it + gq, m * 8)]) = sq[it];
 #pragma unroll
@@ -508,7 +513,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
     const float* __restrict__ g, const float* __restrict__ beta, const int32_t* __restrict__ cu,
     const int32_t* __restrict__ order, const float* initial_state, float* final_state,
     uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale,
-    const int32_t* __restrict__ state_idx, int P) {
+    const int32_t* __restrict__ state_idx, int P, int* fault) {
     constexpr int VW = 16 * NVT;        // value columns per state wave
     constexpr int VB = NS * VW;         // value columns per workgroup
     constexpr int VSPLIT = D / VB;
@@ -636,9 +641,9 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
             // (uniform values, held in scalar registers through the chunk)
             const unsigned rdy_seen = __builtin_amdgcn_readfirstlane(seen_rdy);
             const unsigned hu_seen = __builtin_amdgcn_readfirstlane(seen_hu);
-            wait_seen(&sm.cnt[CNT_STG], (unsigned)(xs + 1), seen_stg);
+            wait_seen(&sm.cnt[CNT_STG], (unsigned)(xs + 1), seen_stg, fault);
             // with output waves: the previous chunk's S0 hi operands were read
-            if constexpr (NO > 0) wait_seen(&sm.cnt[CNT_HAND0 + 4 * wave + 1], (unsigned)xs, seen_hs);
+            if constexpr (NO > 0) wait_seen(&sm.cnt[CNT_HAND0 + 4 * wave + 1], (unsigned)xs, seen_hs, fault);
             // K S0^T (S0 hi + lo), rows t; (Q S0^T)^T (S0 hi), rows v, unless
             // an output wave takes it (it gets the S0 hi operands instead)
             f32x4_t ks[NCT][NVT], ot[NVT][NCT];
@@ -697,7 +702,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
             }
             if constexpr (NO > 0) signal(&sm.cnt[CNT_HAND0 + 4 * wave + 0], lane);
             // W = V - diag(exp(gamma)) K S0^T (in ks)
-            wait_seen(&sm.cnt[CNT_READY0 + xs % NP], (unsigned)(xs / NP + 1), rdy_seen);
+            wait_seen(&sm.cnt[CNT_READY0 + xs % NP], (unsigned)(xs / NP + 1), rdy_seen, fault);
             // T operands of U = T diag(beta) W, read now so that their latency
             // hides behind the vector work of W
             bf16x8_t tah[NCT][2], tal[NCT][2];
@@ -766,7 +771,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
             }
             if constexpr (NO > 0) {
                 // the previous chunk's U hi operands were read
-                wait_seen(&sm.cnt[CNT_HAND0 + 4 * wave + 3], (unsigned)xs, hu_seen);
+                wait_seen(&sm.cnt[CNT_HAND0 + 4 * wave + 3], (unsigned)xs, hu_seen, fault);
 #pragma unroll
                 for (int kc = 0; kc < C; kc += 32)
 #pragma unroll
@@ -903,14 +908,14 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
                 const f32x4_t zero4 = {0.f, 0.f, 0.f, 0.f};
                 // the chunk's Q operands go to registers at once, so that the Q
                 // buffer is released before the S0 operands arrive
-                wait_ge(&sm.cnt[CNT_STG], (unsigned)(xs + 1));
+                wait_ge(&sm.cnt[CNT_STG], (unsigned)(xs + 1), fault);
                 bf16x8_t aq[D / 32][NCT];
 #pragma unroll
                 for (int kq = 0; kq < D / 32; ++kq)
 #pragma unroll
                     for (int ct = 0; ct < NCT; ++ct) aq[kq][ct] = row_frag(sm.qb, 16 * ct + m, 32 * kq, gq);
                 signal(&sm.cnt[CNT_QVFREE], lane);
-                wait_ge(&sm.cnt[CNT_HAND0 + 4 * w + 0], (unsigned)(xs + 1));
+                wait_ge(&sm.cnt[CNT_HAND0 + 4 * w + 0], (unsigned)(xs + 1), fault);
                 bf16x8_t bh[D / 32][NVT];
 #pragma unroll
                 for (int kq = 0; kq < D / 32; ++kq)
@@ -924,7 +929,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
                     for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
                         for (int vt = 0; vt < NVT; ++vt) ot[vt][ct] = mma(bh[kq][vt], aq[kq][ct], kq == 0 ? zero4 : ot[vt][ct]);
-                wait_ge(&sm.cnt[CNT_READY0 + xs % NP], (unsigned)(xs / NP + 1));
+                wait_ge(&sm.cnt[CNT_READY0 + xs % NP], (unsigned)(xs / NP + 1), fault);
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) {
                     const float e = sl.eg[16 * ct + m] * scale;
@@ -939,7 +944,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
                         if (32 * hb > 16 * ct + 15) continue;
                         pf[ct][hb] = blk_frag(sl.pm, sm.zero, ct, 32 * hb, m, gq);
                     }
-                wait_ge(&sm.cnt[CNT_HAND0 + 4 * w + 2], (unsigned)(xs + 1));
+                wait_ge(&sm.cnt[CNT_HAND0 + 4 * w + 2], (unsigned)(xs + 1), fault);
                 bf16x8_t uh[C / 32][NVT];
 #pragma unroll
                 for (int kc = 0; kc < C / 32; ++kc)
@@ -983,7 +988,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
         }
     } else {
         // ======================= producer waves ================================
-        ProdCtx pc = {q, k, v, g, beta, qk_stride, v_stride, 0, 0, 0, 0, H_v, wave - NS - NO, 0, scale};
+        ProdCtx pc = {q, k, v, g, beta, qk_stride, v_stride, 0, 0, 0, 0, H_v, wave - NS - NO, 0, scale, fault};
         // stream chunks x = pw, pw + NP, ...: the work item holding chunk x
         // starts at stream index xbeg
         int pass = 0, xbeg = 0;
@@ -1024,21 +1029,21 @@ int device_compute_units() {
 // One workgroup per compute unit (the LDS use admits one), each walking its
 // work items; fewer items than compute units give one item per workgroup.
 template <int NS, int NVT, int NO>
-static hipError_t launch_pipe(const PrefillArgs& a, const int32_t* order, hipStream_t stream) {
+static hipError_t launch_pipe(const PrefillArgs& a, int32_t* order, hipStream_t stream) {
     constexpr int VSPLIT = pipe::D / (16 * NS * NVT);
     const long items = (long)a.N * a.H_v * VSPLIT;
     const long grid = std::min<long>(items, device_compute_units());
     hipLaunchKernelGGL((pipe::prefill_pipe_kernel<NS, NVT, NO>), dim3((unsigned)grid),
                        dim3(64 * (NS + NO + pipe::NP)), 0, stream, (const uint16_t*)a.q, (const uint16_t*)a.k,
                        (const uint16_t*)a.v, a.g, a.beta, a.cu_seqlens, order, a.initial_state, a.final_state,
-                       (uint16_t*)a.o, a.N, a.H_qk, a.H_v, a.scale, a.state_idx, a.P);
+                       (uint16_t*)a.o, a.N, a.H_qk, a.H_v, a.scale, a.state_idx, a.P, order + a.N + 1);
     return hipGetLastError();
 }
 
 // One workgroup per (sequence, head) when there are enough of them to fill the
 // device; otherwise each head's value columns are split over 2 or 4
 // workgroups (one workgroup per compute unit fits in LDS).
-hipError_t launch_prefill_pipe(const PrefillArgs& a, const int32_t* order, hipStream_t stream) {
+hipError_t launch_prefill_pipe(const PrefillArgs& a, int32_t* order, hipStream_t stream) {
     const long heads = (long)a.N * a.H_v;
     const long cus = device_compute_units();
     if (heads * 4 <= cus) return launch_pipe<2, 1, 2>(a, order, stream);

@@ -72,7 +72,10 @@ __global__ __launch_bounds__(256) void prefill_recur_kernel(
         for (int i = threadIdx.x; i < N; i += blockDim.x) mine += cu[i + 1] - cu[i] > kRecurMax;
         if (mine) atomicAdd(&nlong, mine);
         __syncthreads();
-        if (threadIdx.x == 0) order[N] = nlong;
+        if (threadIdx.x == 0) {
+            order[N] = nlong;
+            order[N + 1] = 0;  // the chunk kernel's wait-fault word
+        }
         return;
     }
     constexpr int ROWS = NWAVE * ROWS_PER_WAVE;

@@ -10,6 +10,26 @@ from paper_2607_17979_amd import workloads as wl
 pytestmark = pytest.mark.gpu
 
 
+def _workspace(N, T, H_qk, H_v, D, dev):
+    """A prefill workspace filled with 0xFF bytes, so that the wait-fault word
+    reads 0 afterwards only if the call cleared it."""
+    import torch
+
+    need = gdn.gdn_prefill_workspace_size(N, T, H_qk, H_v, D, D, gdn.default_chunk(D))
+    return torch.full((max(need, 256),), 255, dtype=torch.uint8, device=dev)
+
+
+def _assert_no_wait_fault(ws, N):
+    """Word N + 1 of the workspace is set if a wave of the chunk kernel gave up
+    one of its bounded waits (its results would then be invalid)."""
+    import torch
+
+    if N == 0:
+        return  # a no-op call leaves the workspace alone
+    torch.cuda.synchronize()
+    assert int(ws.view(torch.int32)[N + 1].item()) == 0, "a chunk-kernel wait ran out of its bound"
+
+
 def _prefill_gpu(inp, dev, scale=None, in_place=False, workspace=None):
     import torch
 
@@ -24,8 +44,11 @@ def _prefill_gpu(inp, dev, scale=None, in_place=False, workspace=None):
     else:
         fin = torch.full((N, H_v, D, D), float("nan"), dtype=torch.float32, device=dev)
     o = torch.full((T, H_v, D), float("nan"), dtype=torch.bfloat16, device=dev)
+    if workspace is None:
+        workspace = _workspace(N, T, H_qk, H_v, D, dev)
     gdn.gdn_prefill_varlen(q, k, v, g, b, cu, init, fin, o,
                            scale=inp.scale if scale is None else scale, workspace=workspace)
+    _assert_no_wait_fault(workspace, N)
     return o, fin
 
 
@@ -151,20 +174,23 @@ def test_prefill_gva_equals_repeated_heads_bitwise():
 
 def test_prefill_schedule_is_longest_first():
     """The workspace holds the sequence order, longest first, ties by index,
-    then the count of sequences run in chunks (integer work: compared exactly)."""
+    then the count of sequences run in chunks, then the cleared wait-fault
+    word (integer work: compared exactly)."""
     import torch
 
     dev = device()
     lengths = [5, 130, 0, 130, 64, 1, 300, 5]
     inp = wl.prefill_inputs(43, lengths, 1, 2, 128)
-    ws = torch.zeros(256, dtype=torch.uint8, device=dev)
+    ws = torch.full((256,), 255, dtype=torch.uint8, device=dev)
     _prefill_gpu(inp, dev, workspace=ws)
     torch.cuda.synchronize()
-    words = ws.view(torch.int32)[:len(lengths) + 1].cpu().numpy()
-    expect = sorted(range(len(lengths)), key=lambda i: (-lengths[i], i))
-    assert words[:-1].tolist() == expect
+    N = len(lengths)
+    words = ws.view(torch.int32)[:N + 2].cpu().numpy()
+    expect = sorted(range(N), key=lambda i: (-lengths[i], i))
+    assert words[:N].tolist() == expect
     # then the number of sequences run in chunks (longer than 8 tokens)
-    assert words[-1] == sum(n > 8 for n in lengths)
+    assert words[N] == sum(n > 8 for n in lengths)
+    assert words[N + 1] == 0
 
 
 def test_prefill_then_decode_continues_the_sequence():
@@ -349,7 +375,9 @@ def test_prefill_indexed_pool(D):
     g, b, cu = to_dev(inp.g, dev), to_dev(inp.beta, dev), to_dev(inp.cu_seqlens, dev)
     pool = to_dev(pool_host, dev)
     o = torch.full((inp.q.shape[0], 4, D), float("nan"), dtype=torch.bfloat16, device=dev)
-    gdn.gdn_prefill_varlen_indexed(q, k, v, g, b, cu, pool, to_dev(slots, dev), o)
+    ws = _workspace(len(lengths), int(sum(lengths)), 2, 4, D, dev)
+    gdn.gdn_prefill_varlen_indexed(q, k, v, g, b, cu, pool, to_dev(slots, dev), o, workspace=ws)
+    _assert_no_wait_fault(ws, len(lengths))
     # the same sequences with gdn_prefill_varlen on the gathered states
     init_host = np.stack([pool_host[s] if ok else np.zeros_like(pool_host[0]) for s, ok in zip(slots, valid)])
     init = to_dev(init_host, dev)
@@ -397,7 +425,9 @@ def test_prefill_indexed_pool_many_short_sequences():
     g, b, cu = to_dev(inp.g, dev), to_dev(inp.beta, dev), to_dev(inp.cu_seqlens, dev)
     pool = to_dev(pool_host, dev)
     o = torch.full((inp.q.shape[0], 4, D), float("nan"), dtype=torch.bfloat16, device=dev)
-    gdn.gdn_prefill_varlen_indexed(q, k, v, g, b, cu, pool, to_dev(slots, dev), o)
+    ws = _workspace(N, int(sum(lengths)), 2, 4, D, dev)
+    gdn.gdn_prefill_varlen_indexed(q, k, v, g, b, cu, pool, to_dev(slots, dev), o, workspace=ws)
+    _assert_no_wait_fault(ws, N)
     init_host = np.where(valid[:, None, None, None], pool_host[np.maximum(slots, 0)], 0.0).astype(np.float32)
     init = to_dev(init_host, dev)
     fin = torch.empty_like(init)
