@@ -329,9 +329,9 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args(argv)
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the "
-              "per-GPU kernels shard by (sequence, head) with no exchange, see the design notes",
-              file=sys.stderr)
+        print(f"bench.py: the library runs on one GPU (asked for --gpus {args.gpus}); its "
+              "kernels would shard by (sequence, head) across GPUs with no exchange, which is "
+              "not built", file=sys.stderr)
         return 2
 
     import torch
