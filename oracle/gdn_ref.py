@@ -17,7 +17,7 @@ Definitions", subsection "Gated Delta Net"):
   place) and prefill (a whole packed sequence, returning every output and the
   final state).
 
-Readings where the paper is silent (each is listed in the design notes):
+Readings where the paper is silent:
   * S is d_v x d_k and stored [.., d_v, d_k] with the k index contiguous;
     o_t = S_t q_t uses the state *after* the update.
   * one gate g and one beta per (token, value head); beta is post-sigmoid.
