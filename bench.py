@@ -156,12 +156,13 @@ class DecodeIndexed:
 
 
 class MultiToken:
-    """A multi-token decode step through gdn_prefill_varlen: ``N`` sequences of
-    ``len`` new tokens each, states updated in place (initial_state is
-    final_state).  ``per_step`` launches per call, each on the next of ``nbuf``
-    state buffers, as for Decode."""
+    """A multi-token decode step: ``N`` sequences of ``len`` new tokens each,
+    states updated in place, through gdn_decode_multitoken (``via_prefill``
+    False) or gdn_prefill_varlen with initial_state is final_state.
+    ``per_step`` launches per call, each on the next of ``nbuf`` state
+    buffers, as for Decode."""
 
-    def __init__(self, dev, w, nbuf=4, per_step=4):
+    def __init__(self, dev, w, nbuf=4, per_step=4, via_prefill=False):
         import torch
         from paper_2607_17979_amd import gdn
         from paper_2607_17979_amd import workloads as wl
@@ -178,6 +179,7 @@ class MultiToken:
         self.chunk = w["chunk"]
         self.i = 0
         self.per_step = per_step
+        self.via_prefill = via_prefill
         self.bytes = prefill_bytes(self.T, self.N, self.H_qk, self.H_v, self.D, True)
 
     def __call__(self):
@@ -186,8 +188,12 @@ class MultiToken:
         x = self.x
         for _ in range(self.per_step):
             st = self.states[self.i % len(self.states)]
-            gdn.gdn_prefill_varlen(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], st, st, self.o,
-                                   chunk=self.chunk, workspace=self.ws)
+            if self.via_prefill:
+                gdn.gdn_prefill_varlen(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], st, st, self.o,
+                                       chunk=self.chunk, workspace=self.ws)
+            else:
+                gdn.gdn_decode_multitoken(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], st, self.o,
+                                          workspace=self.ws)
             self.i += 1
 
 
@@ -398,17 +404,23 @@ def main(argv=None):
 
     if args.workload == "decode_multitoken":
         mt = MultiToken(dev, W["decode_multitoken"])
+        # the same step through gdn_prefill_varlen (one more launch, which finds
+        # nothing to do), timed first, for comparison
+        mtp = MultiToken(dev, W["decode_multitoken"], via_prefill=True)
+        _, per_p = _time_parts([mtp], args.steps, args.warmup)
         ms_step, per = _time_parts([mt], args.steps, args.warmup)
         t = per[0] * 1e-3 / mt.per_step
         gbs = mt.bytes / t / 1e9
         out.update(value=gbs, unit="GB/s", ms_per_step=ms_step, dtype="f32",
                    tokens_per_s=mt.T / t, us_per_launch=t * 1e6,
+                   us_per_call_via_prefill_varlen=per_p[0] * 1e3 / mtp.per_step,
                    roofline=dict(bound="hbm", achieved=gbs, peak=HBM_PEAK_GBS, unit="GB/s",
                                  frac=gbs / HBM_PEAK_GBS, traffic=None,
                                  kernel="gdn::recur::prefill_recur_kernel (token by token; "
                                         "sequences of at most 8 tokens)",
                                  bytes_per_launch=mt.bytes),
-                   config=dict(workload="decode_multitoken", N=mt.N, tokens_per_sequence=mt.Tn,
+                   config=dict(workload="decode_multitoken (gdn_decode_multitoken)", N=mt.N,
+                               tokens_per_sequence=mt.Tn,
                                H_qk=mt.H_qk, H_v=mt.H_v, d=mt.D, state_buffers=len(mt.states),
                                launches_per_step=mt.per_step, in_place=True))
         print(json.dumps(out), flush=True)

@@ -149,11 +149,11 @@ GDN_API size_t gdn_prefill_workspace_size(int N, int T, int H_qk, int H_v,
  *                  gdn_prefill_workspace_size(...) bytes, 256-byte aligned;
  *                  its contents are scratch (overwritten by each call).  Once
  *                  the call has completed on the stream, int32 word N + 1 of
- *                  it is 0, or nonzero if a wave of the chunk kernel gave up
- *                  one of its bounded waits for another wave (a broken
- *                  synchronisation, never expected): the call's results are
- *                  then invalid.  A diagnostic read, not a status the call
- *                  returns (the call does not wait for its kernels).
+ *                  it is 0, or has bit 0 set if a wave of the chunk kernel
+ *                  gave up one of its bounded waits for another wave (a
+ *                  broken synchronisation, never expected): the call's
+ *                  results are then invalid.  A diagnostic read, not a status
+ *                  the call returns (the call does not wait for its kernels).
  *
  * For D = 128, sequences of at most 8 tokens are computed token by token in
  * fp32 (the decode arithmetic), longer ones in chunks; the choice depends
@@ -204,6 +204,38 @@ GDN_API int gdn_prefill_varlen_indexed(const void* q, const void* k, const void*
                        void* o,
                        int N, int T, int P, int H_qk, int H_v, int D_k, int D_v,
                        int chunk, float scale,
+                       void* workspace, size_t workspace_bytes,
+                       void* stream);
+
+/*
+ * gdn_decode_multitoken -- a decode step of a few new tokens per sequence
+ * (the decode regime with n <= 8 updates per state, the state updated in
+ * place): the recurrence of gdn_prefill_varlen for sequences the caller
+ * promises are at most 8 tokens long.  It runs only the token-by-token
+ * kernel, sparing gdn_prefill_varlen's second launch, which that call cannot
+ * rule out because it never reads cu_seqlens on the host.  Results equal
+ * gdn_prefill_varlen with initial_state == final_state == state bit for bit,
+ * and hence n calls of gdn_decode.
+ *
+ *   q, k, v, g, beta, cu_seqlens, o, scale   as gdn_prefill_varlen (D = 128)
+ *   state      fp32 [N, H_v, D, D], read and overwritten IN PLACE
+ *   workspace  gdn_prefill_workspace_size(N, T, H_qk, H_v, 128, 128, 64)
+ *              bytes, 256-byte aligned.  After the call has completed, bit 1
+ *              of int32 word N + 1 is set if some sequence was longer than 8
+ *              tokens: such a sequence is skipped (its state and output rows
+ *              are left as they were); the others are computed normally.
+ *
+ * N = 0 is a no-op returning GDN_OK.  GDN_EUNSUPPORTED unless D_k = D_v =
+ * 128; GDN_EINVAL for T > 8 N (some sequence is then necessarily longer),
+ * N * H_v > 2^30, a NULL state or cu_seqlens; other errors as
+ * gdn_prefill_varlen.
+ */
+GDN_API int gdn_decode_multitoken(const void* q, const void* k, const void* v,
+                       const float* g, const float* beta,
+                       const int32_t* cu_seqlens,
+                       float* state, void* o,
+                       int N, int T, int H_qk, int H_v, int D_k, int D_v,
+                       float scale,
                        void* workspace, size_t workspace_bytes,
                        void* stream);
 

@@ -146,7 +146,7 @@ int gdn_prefill_varlen(const void* q, const void* k, const void* v, const float*
                     workspace_bytes, workspace == nullptr ? " (NULL)" : "");
     if (!aligned(workspace, 256)) return fail(GDN_EALIGN, "workspace is not 256-byte aligned");
     gdn::PrefillArgs a{q, k, v, g, beta, cu_seqlens, initial_state, final_state, o,
-                       N, T, H_qk, H_v, D_k, chunk, scale, workspace, nullptr, 0};
+                       N, T, H_qk, H_v, D_k, chunk, scale, workspace, nullptr, 0, false};
     hipError_t e = gdn::launch_prefill(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail(GDN_EHIP, "prefill launch failed: %s", hipGetErrorString(e));
     return GDN_OK;
@@ -184,9 +184,42 @@ int gdn_prefill_varlen_indexed(const void* q, const void* k, const void* v, cons
                     workspace_bytes, workspace == nullptr ? " (NULL)" : "");
     if (!aligned(workspace, 256)) return fail(GDN_EALIGN, "workspace is not 256-byte aligned");
     gdn::PrefillArgs a{q, k, v, g, beta, cu_seqlens, state_pool, state_pool, o,
-                       N, T, H_qk, H_v, D_k, chunk, scale, workspace, state_idx, P};
+                       N, T, H_qk, H_v, D_k, chunk, scale, workspace, state_idx, P, false};
     hipError_t e = gdn::launch_prefill(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail(GDN_EHIP, "prefill launch failed: %s", hipGetErrorString(e));
+    return GDN_OK;
+}
+
+int gdn_decode_multitoken(const void* q, const void* k, const void* v, const float* g,
+                          const float* beta, const int32_t* cu_seqlens, float* state, void* o, int N,
+                          int T, int H_qk, int H_v, int D_k, int D_v, float scale, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+    g_last_error.clear();
+    if (N < 0 || T < 0) return fail(GDN_EINVAL, "N and T must be >= 0 (N=%d, T=%d)", N, T);
+    if (int st = check_heads(H_qk, H_v, D_k, D_v)) return st;
+    if (D_k != 128) return fail(GDN_EUNSUPPORTED, "multi-token decode runs for head dim 128 (got %d)", D_k);
+    if ((long long)T > (long long)gdn::kRecurMax * N)
+        return fail(GDN_EINVAL, "T = %d > %d N: some sequence has more than %d tokens", T, gdn::kRecurMax,
+                    gdn::kRecurMax);
+    if (N == 0) return GDN_OK;
+    if ((long long)N * H_v > (1LL << 30))
+        return fail(GDN_EINVAL, "problem too large (N=%d, H_v=%d)", N, H_v);
+    int st;
+    if ((st = check_ptr4(cu_seqlens, "cu_seqlens")) || (st = check_ptr16(state, "state"))) return st;
+    if (T > 0) {
+        if ((st = check_ptr16(q, "q")) || (st = check_ptr16(k, "k")) || (st = check_ptr16(v, "v")) ||
+            (st = check_ptr16(o, "o")) || (st = check_ptr4(g, "g")) || (st = check_ptr4(beta, "beta")))
+            return st;
+    }
+    const size_t need = gdn::prefill_workspace_bytes(N);
+    if (workspace == nullptr || workspace_bytes < need)
+        return fail(GDN_EWORKSPACE, "workspace of %zu bytes needed, %zu given%s", need,
+                    workspace_bytes, workspace == nullptr ? " (NULL)" : "");
+    if (!aligned(workspace, 256)) return fail(GDN_EALIGN, "workspace is not 256-byte aligned");
+    gdn::PrefillArgs a{q, k, v, g, beta, cu_seqlens, state, state, o,
+                       N, T, H_qk, H_v, D_k, chunk_for(D_k), scale, workspace, nullptr, 0, true};
+    hipError_t e = gdn::launch_prefill(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(GDN_EHIP, "multi-token decode launch failed: %s", hipGetErrorString(e));
     return GDN_OK;
 }
 

@@ -37,6 +37,9 @@ struct PrefillArgs {
     void* workspace;
     const int32_t* state_idx;  // NULL: state n is sequence n; else a pool slot per sequence
     int P;                     // pool slots (with state_idx)
+    bool short_only;           // the caller's promise that no sequence exceeds kRecurMax:
+                               // only the token-by-token launch runs, and a longer sequence
+                               // is skipped and flagged (wait-fault word bit 1)
 };
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
@@ -58,9 +61,9 @@ int device_compute_units();
 // Workspace layout of the prefill: int32 order[N] (sequence indices sorted by
 // length, longest first, ties by index), then (d = 128) int32 order[N] = the
 // number of sequences longer than kRecurMax, then int32 order[N + 1] = the
-// wait-fault word (cleared by the call's first launch, set by any wave of the
-// chunk kernel whose counter wait ran out of its bound); rounded up to 256
-// bytes.
+// fault word (cleared by the call's first launch; bit 0 set by any wave of the
+// chunk kernel whose counter wait ran out of its bound, bit 1 by a short-only
+// call that met a longer sequence); rounded up to 256 bytes.
 size_t prefill_workspace_bytes(int N);
 
 }  // namespace gdn

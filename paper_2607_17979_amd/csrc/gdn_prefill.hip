@@ -490,7 +490,7 @@ hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {
         // short sequences token by token (that launch also writes the
         // schedule), the rest in chunks; with T <= kRecurMax every sequence is short
         hipError_t e = launch_prefill_recur(a, order, stream);
-        if (e != hipSuccess || a.T <= kRecurMax) return e;
+        if (e != hipSuccess || a.T <= kRecurMax || a.short_only) return e;
         return launch_prefill_pipe(a, order, stream);
     }
     hipLaunchKernelGGL(prefill_schedule_kernel, dim3(1), dim3(256), 0, stream, a.cu_seqlens, a.N, order);

@@ -60,12 +60,13 @@ __global__ __launch_bounds__(256) void prefill_recur_kernel(
     const float* __restrict__ g, const float* __restrict__ beta, const int32_t* __restrict__ cu,
     int32_t* __restrict__ order, const float* initial_state, float* final_state,
     uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale,
-    const int32_t* __restrict__ state_idx, int P) {
+    const int32_t* __restrict__ state_idx, int P, int short_only) {
     __shared__ Smem sm;
     __shared__ int nlong;
     if (blockIdx.x == 0) {
-        // the chunk kernel's schedule, then the number of sequences it runs
-        schedule_longest_first(cu, N, order, sm.sched_len);
+        // the chunk kernel's schedule (not needed when no chunk kernel
+        // follows), then the number of sequences it runs
+        if (!short_only) schedule_longest_first(cu, N, order, sm.sched_len);
         if (threadIdx.x == 0) nlong = 0;
         __syncthreads();
         int mine = 0;
@@ -74,7 +75,9 @@ __global__ __launch_bounds__(256) void prefill_recur_kernel(
         __syncthreads();
         if (threadIdx.x == 0) {
             order[N] = nlong;
-            order[N + 1] = 0;  // the chunk kernel's wait-fault word
+            // the fault word: a short-only call that met a longer sequence
+            // (skipped) sets bit 1; the chunk kernel may set bit 0 later
+            order[N + 1] = (short_only && nlong > 0) ? 2 : 0;
         }
         return;
     }
@@ -237,7 +240,7 @@ hipError_t launch_prefill_recur(const PrefillArgs& a, int32_t* order, hipStream_
     hipLaunchKernelGGL(recur::prefill_recur_kernel, dim3((unsigned)grid), dim3(64 * recur::NWAVE), 0, stream,
                        (const uint16_t*)a.q, (const uint16_t*)a.k, (const uint16_t*)a.v, a.g, a.beta,
                        a.cu_seqlens, order, a.initial_state, a.final_state, (uint16_t*)a.o, a.N, a.H_qk,
-                       a.H_v, a.scale, a.state_idx, a.P);
+                       a.H_v, a.scale, a.state_idx, a.P, a.short_only ? 1 : 0);
     return hipGetLastError();
 }
 

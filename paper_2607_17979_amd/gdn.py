@@ -24,11 +24,13 @@ __all__ = [
     "gdn_prefill_workspace_size",
     "gdn_prefill_varlen",
     "gdn_prefill_varlen_indexed",
+    "gdn_decode_multitoken",
     "EXPORTED_SYMBOLS",
 ]
 
 EXPORTED_SYMBOLS = ("gdn_last_error", "gdn_abi_version", "gdn_decode", "gdn_decode_indexed",
-                    "gdn_prefill_workspace_size", "gdn_prefill_varlen", "gdn_prefill_varlen_indexed")
+                    "gdn_prefill_workspace_size", "gdn_prefill_varlen", "gdn_prefill_varlen_indexed",
+                    "gdn_decode_multitoken")
 
 _STATUS = {0: "GDN_OK", -1: "GDN_EINVAL", -2: "GDN_EUNSUPPORTED", -3: "GDN_EALIGN",
            -4: "GDN_EWORKSPACE", -5: "GDN_EHIP"}
@@ -72,6 +74,9 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.gdn_prefill_varlen_indexed.restype = ci
     lib.gdn_prefill_varlen_indexed.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                                ci, ci, ci, ci, ci, ci, ci, ci, cf, vp, sz, vp]
+    lib.gdn_decode_multitoken.restype = ci
+    lib.gdn_decode_multitoken.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp,
+                                          ci, ci, ci, ci, ci, ci, cf, vp, sz, vp]
     if path is None:
         _lib = lib
     return lib
@@ -251,3 +256,36 @@ def gdn_prefill_varlen_indexed(q, k, v, g, beta, cu_seqlens, state_pool, state_i
                                           _ptr(o), N, T, P, H_qk, H_v, D, D, chunk, float(scale),
                                           _ptr(workspace), workspace.numel() * workspace.element_size(),
                                           _stream(q, stream)))
+
+
+def gdn_decode_multitoken(q, k, v, g, beta, cu_seqlens, state, o, scale: float = 1.0,
+                          workspace=None, stream=None) -> None:
+    """Decode step of at most 8 new tokens per sequence, state in place (see
+    include/gdn.h).  q, k: bf16 [T, H_qk, 128]; v: bf16 [T, H_v, 128]; g, beta:
+    fp32 [T, H_v]; cu_seqlens: int32 [N + 1] on the device; state: fp32
+    [N, H_v, 128, 128]; o: bf16 [T, H_v, 128].  ``workspace`` (uint8, at least
+    gdn_prefill_workspace_size bytes) is allocated with torch when omitted."""
+    import torch
+
+    T, H_qk, D = q.shape
+    H_v = v.shape[1]
+    N = cu_seqlens.shape[0] - 1
+    dev = q.device
+    if dev.type != "cuda":
+        raise ValueError("tensors must be on a GPU device")
+    _need(q, "q", torch.bfloat16, (T, H_qk, D), dev)
+    _need(k, "k", torch.bfloat16, (T, H_qk, D), dev)
+    _need(v, "v", torch.bfloat16, (T, H_v, D), dev)
+    _need(g, "g", torch.float32, (T, H_v), dev)
+    _need(beta, "beta", torch.float32, (T, H_v), dev)
+    _need(cu_seqlens, "cu_seqlens", torch.int32, (N + 1,), dev)
+    _need(state, "state", torch.float32, (N, H_v, D, D), dev)
+    _need(o, "o", torch.bfloat16, (T, H_v, D), dev)
+    need = gdn_prefill_workspace_size(N, T, H_qk, H_v, D, D, default_chunk(D))
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    lib = load_library()
+    _check(lib.gdn_decode_multitoken(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(cu_seqlens),
+                                     _ptr(state), _ptr(o), N, T, H_qk, H_v, D, D, float(scale),
+                                     _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                     _stream(q, stream)))

@@ -195,3 +195,31 @@ def test_prefill_indexed_empty_is_noop(lib):
     assert prefill_indexed(lib, q=None, k=None, v=None, g=None, beta=None, cu=None, pool=None, idx=None,
                            o=None, N=0, T=0, ws=None, ws_bytes=0) == OK
     assert prefill_indexed(lib, pool=None, idx=None, Pn=0) == OK
+
+
+def multitoken(lib, q=P, k=P, v=P, g=P, beta=P, cu=P, state=P, o=P, N=3, T=10, H_qk=1, H_v=2,
+               Dk=128, Dv=128, ws=P, ws_bytes=256):
+    return lib.gdn_decode_multitoken(q, k, v, g, beta, cu, state, o, N, T, H_qk, H_v, Dk, Dv, 1.0,
+                                     ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(N=-1), EINVAL, "must be >= 0"),
+    (dict(H_qk=2, H_v=3), EINVAL, "multiple"),
+    (dict(Dk=16, Dv=16), EUNSUP, "head dim 128"),
+    (dict(T=25), EINVAL, "more than 8 tokens"),
+    (dict(cu=None), EINVAL, "cu_seqlens is NULL"),
+    (dict(state=None), EINVAL, "state is NULL"),
+    (dict(state=P + 8), EALIGN, "state"),
+    (dict(q=None), EINVAL, "q is NULL"),
+    (dict(ws=None), EWS, "workspace"),
+    (dict(ws=P + 16), EALIGN, "workspace"),
+])
+def test_decode_multitoken_rejects(lib, kw, status, msg):
+    assert multitoken(lib, **kw) == status
+    assert msg in gdn.gdn_last_error()
+
+
+def test_decode_multitoken_empty_is_noop(lib):
+    assert multitoken(lib, q=None, k=None, v=None, g=None, beta=None, cu=None, state=None, o=None,
+                      N=0, T=0, ws=None, ws_bytes=0) == OK

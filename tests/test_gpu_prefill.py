@@ -329,6 +329,53 @@ def test_multi_token_decode_equals_decode_steps_bitwise():
     _full_oracle_check(inp, o1, f1, "multi-token decode")
 
 
+def test_decode_multitoken_entry_point():
+    """gdn_decode_multitoken (only the token-by-token launch) equals
+    gdn_prefill_varlen in place bit for bit on 0..8-token sequences, with the
+    fault word clear.  A batch that also holds a 9-token sequence: that
+    sequence is skipped (its state and output rows untouched) and bit 1 of the
+    fault word is set; every other sequence is computed as before."""
+    import torch
+
+    dev = device()
+    lengths = [4, 0, 8, 1, 3, 8, 2, 5]
+    H_qk, H_v, D = 16, 32, 128
+    N, T = len(lengths), sum(lengths)
+    note(f"multi-token entry point, lengths {lengths}")
+    inp = wl.prefill_inputs(55, lengths, H_qk, H_v, D, state_std=0.02)
+    o_ref, f_ref = _prefill_gpu(inp, dev, in_place=True)
+    q, k, v = (to_dev(x, dev, bf16=True) for x in (inp.q, inp.k, inp.v))
+    g, b, cu = to_dev(inp.g, dev), to_dev(inp.beta, dev), to_dev(inp.cu_seqlens, dev)
+    st = to_dev(inp.initial_state, dev)
+    o = torch.full((T, H_v, D), float("nan"), dtype=torch.bfloat16, device=dev)
+    ws = _workspace(N, T, H_qk, H_v, D, dev)
+    gdn.gdn_decode_multitoken(q, k, v, g, b, cu, st, o, workspace=ws)
+    _assert_no_wait_fault(ws, N)
+    assert torch.equal(o.view(torch.int16), o_ref.view(torch.int16))
+    assert torch.equal(st.view(torch.int32), f_ref.view(torch.int32))
+
+    # one sequence of 9 tokens: skipped and flagged
+    lengths2 = [3, 9, 2, 6]
+    N2, T2 = len(lengths2), sum(lengths2)
+    inp2 = wl.prefill_inputs(56, lengths2, H_qk, H_v, D, state_std=0.02)
+    q, k, v = (to_dev(x, dev, bf16=True) for x in (inp2.q, inp2.k, inp2.v))
+    g, b, cu = to_dev(inp2.g, dev), to_dev(inp2.beta, dev), to_dev(inp2.cu_seqlens, dev)
+    st = to_dev(inp2.initial_state, dev)
+    o = torch.full((T2, H_v, D), float("nan"), dtype=torch.bfloat16, device=dev)
+    ws = _workspace(N2, T2, H_qk, H_v, D, dev)
+    gdn.gdn_decode_multitoken(q, k, v, g, b, cu, st, o, workspace=ws)
+    torch.cuda.synchronize()
+    assert int(ws.view(torch.int32)[N2 + 1].item()) == 2
+    long_rows = slice(3, 12)
+    assert torch.isnan(o[long_rows].float()).all()
+    assert np.array_equal(st[1].cpu().numpy(), inp2.initial_state[1])
+    o_ref2, s_ref2 = ref.prefill_varlen(inp2.q, inp2.k, inp2.v, inp2.g, inp2.beta, inp2.cu_seqlens,
+                                        inp2.initial_state, scale=inp2.scale)
+    keep = np.r_[0:3, 12:T2]
+    check_outputs(bf16_np(o)[keep], o_ref2[keep], "multi-token entry, short sequences")
+    check_states(st.cpu().numpy()[[0, 2, 3]], s_ref2[[0, 2, 3]], "multi-token entry, short sequences")
+
+
 def test_prefill_many_short_sequences():
     """The short-sequence regime at the bench's head layout: 64 sequences of
     8 tokens, 32 value / 16 q/k heads, nonzero states (sampled units)."""
