@@ -153,7 +153,9 @@ GDN_API size_t gdn_prefill_workspace_size(int N, int T, int H_qk, int H_v,
  *                  gave up one of its bounded waits for another wave (a
  *                  broken synchronisation, never expected): the call's
  *                  results are then invalid.  A diagnostic read, not a status
- *                  the call returns (the call does not wait for its kernels).
+ *                  the call returns (the call does not wait for its kernels);
+ *                  a call that is a no-op (N = 0) leaves the workspace as it
+ *                  was.
  *
  * For D = 128, sequences of at most 8 tokens are computed token by token in
  * fp32 (the decode arithmetic), longer ones in chunks; the choice depends
