@@ -200,6 +200,40 @@ def prefill_inputs(seed: int, lengths: Sequence[int], H_qk: int, H_v: int, D: in
     return PrefillInputs(q, k, v, g, beta, cu.astype(np.int32), init, scale)
 
 
+def prefill_inputs_device(seed: int, N: int, L: int, H_qk: int, H_v: int, D: int,
+                          state_std: float, device):
+    """An equal-length packed batch (N sequences of L tokens) drawn on the GPU
+    with torch's seeded generator, for sizes whose host draw would take
+    minutes; the same distributions as prefill_inputs: q, k N(0, 1)
+    L2-normalised per head in fp32, then rounded to bf16; v N(0, 1) in bf16;
+    beta = sigmoid(N(0, 1)); g = -softplus(N(0, 1)); initial state
+    N(0, state_std^2).  Returns a dict of device tensors (q, k, v, g, beta,
+    init, cu)."""
+    import torch
+
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    T = N * L
+
+    def normal(shape):
+        return torch.randn(shape, generator=gen, device=device, dtype=torch.float32)
+
+    q = torch.empty((T, H_qk, D), dtype=torch.bfloat16, device=device)
+    k = torch.empty_like(q)
+    v = torch.empty((T, H_v, D), dtype=torch.bfloat16, device=device)
+    for t0 in range(0, T, L):  # one sequence at a time: the fp32 draws stay small
+        for dst, H, unit in ((q, H_qk, True), (k, H_qk, True), (v, H_v, False)):
+            x = normal((L, H, D))
+            if unit:
+                x = x / x.norm(dim=-1, keepdim=True)
+            dst[t0:t0 + L] = x.to(torch.bfloat16)
+    beta = torch.sigmoid(normal((T, H_v)))
+    g = -torch.nn.functional.softplus(normal((T, H_v)))
+    init = state_std * normal((N, H_v, D, D))
+    cu = torch.arange(N + 1, dtype=torch.int32, device=device) * L
+    return dict(q=q, k=k, v=v, g=g, beta=beta, init=init, cu=cu)
+
+
 # The five synthetic workloads (sizes and distributions as described in the
 # module docstring).  Values are plain dicts so both sides can read them.
 WORKLOADS = {

@@ -133,6 +133,43 @@ def test_prefill_long_2x64k():
     _sampled_check(inp, o, fin, units, "long 2x64k")
 
 
+def test_prefill_maximum_size():
+    """T * H_v = 2^24, the largest problem the entry point accepts (v and o are
+    then 4 GiB, so byte offsets near their end need 32 bits): 8 sequences x
+    65,536 tokens x 32 value heads, inputs drawn on the device by torch's
+    seeded generator.  The oracle follows the first and the last (sequence,
+    head) unit, the one at the highest addresses, over all their tokens; the
+    fault word is clear."""
+    import torch
+
+    dev = device()
+    N, L, H_qk, H_v, D = 8, 65536, 16, 32, 128
+    T = N * L
+    assert T * H_v == 1 << 24
+    note(f"prefill maximum size: N={N} x {L} tokens, H_v={H_v} (T * H_v = 2^24)")
+    x = wl.prefill_inputs_device(62, N, L, H_qk, H_v, D, 0.02, dev)
+    fin = torch.empty_like(x["init"])
+    o = torch.empty((T, H_v, D), dtype=torch.bfloat16, device=dev)
+    ws = _workspace(N, T, H_qk, H_v, D, dev)
+    gdn.gdn_prefill_varlen(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], x["init"], fin, o,
+                           workspace=ws)
+    _assert_no_wait_fault(ws, N)
+
+    def bits(t):
+        return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+    for n, h in ((0, 0), (N - 1, H_v - 1)):
+        rows = slice(n * L, (n + 1) * L)
+        hq = h * H_qk // H_v
+        note(f"  oracle on unit (sequence {n}, head {h}), {L} tokens")
+        o_ref, s_ref = ref.prefill_varlen(
+            bits(x["q"][rows, hq:hq + 1]), bits(x["k"][rows, hq:hq + 1]), bits(x["v"][rows, h:h + 1]),
+            x["g"][rows, h:h + 1].cpu().numpy(), x["beta"][rows, h:h + 1].cpu().numpy(),
+            np.array([0, L], np.int32), x["init"][n:n + 1, h:h + 1].cpu().numpy())
+        check_outputs(bits(o[rows, h:h + 1]), o_ref, f"maximum size, unit ({n}, {h})")
+        check_states(fin[n:n + 1, h:h + 1].cpu().numpy(), s_ref, f"maximum size, unit ({n}, {h})")
+
+
 def test_prefill_identity_gate_bitwise_and_zero_length():
     """g = 0, beta = 0 leaves every state bit for bit; a zero-length sequence
     returns its initial state bit for bit."""
