@@ -229,9 +229,37 @@ def prefill_inputs_device(seed: int, N: int, L: int, H_qk: int, H_v: int, D: int
             dst[t0:t0 + L] = x.to(torch.bfloat16)
     beta = torch.sigmoid(normal((T, H_v)))
     g = -torch.nn.functional.softplus(normal((T, H_v)))
-    init = state_std * normal((N, H_v, D, D))
+    init = torch.empty((N, H_v, D, D), dtype=torch.float32, device=device)
+    for n0 in range(0, N, 256):  # in slices: no second full-size temporary
+        init[n0:n0 + 256] = state_std * normal((min(256, N - n0), H_v, D, D))
     cu = torch.arange(N + 1, dtype=torch.int32, device=device) * L
     return dict(q=q, k=k, v=v, g=g, beta=beta, init=init, cu=cu)
+
+
+def decode_inputs_device(seed: int, B: int, H_qk: int, H_v: int, D: int, state_std: float,
+                         device):
+    """One decode step's inputs drawn on the GPU with torch's seeded generator
+    (for states of many GiB), with the distributions of decode_inputs.
+    Returns a dict of device tensors (q, k, v, g, beta, state)."""
+    import torch
+
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+
+    def normal(shape):
+        return torch.randn(shape, generator=gen, device=device, dtype=torch.float32)
+
+    q = normal((B, H_qk, D))
+    k = normal((B, H_qk, D))
+    q = (q / q.norm(dim=-1, keepdim=True)).to(torch.bfloat16)
+    k = (k / k.norm(dim=-1, keepdim=True)).to(torch.bfloat16)
+    v = normal((B, H_v, D)).to(torch.bfloat16)
+    beta = torch.sigmoid(normal((B, H_v)))
+    g = -torch.nn.functional.softplus(normal((B, H_v)))
+    state = torch.empty((B, H_v, D, D), dtype=torch.float32, device=device)
+    for b0 in range(0, B, 256):  # in slices: no second full-size temporary
+        state[b0:b0 + 256] = state_std * normal((min(256, B - b0), H_v, D, D))
+    return dict(q=q, k=k, v=v, g=g, beta=beta, state=state)
 
 
 # The five synthetic workloads (sizes and distributions as described in the

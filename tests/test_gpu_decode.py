@@ -279,3 +279,32 @@ def test_decode_indexed_pool():
                               pool_host[slots[valid]])
     check_outputs(bf16_np(o[vi]), o_ref, "indexed")
     check_states(pool_np[slots[valid]], s_ref, "indexed")
+
+
+def test_decode_state_beyond_4gib():
+    """Batch 4,096 x 32 value heads: 8 GiB of fp32 state, so byte offsets into
+    it need more than 32 bits past the first half.  Inputs drawn on the device
+    by torch's seeded generator; the oracle checks the first (batch, head)
+    unit and the one at the highest addresses."""
+    import torch
+
+    dev = device()
+    B, H_qk, H_v, D = 4096, 16, 32, 128
+    note(f"decode state beyond 4 GiB: B={B}, H_v={H_v} ({B * H_v * D * D * 4 / 2**30:.0f} GiB)")
+    x = wl.decode_inputs_device(71, B, H_qk, H_v, D, 0.02, dev)
+    units = ((0, 0), (B - 1, H_v - 1))
+    before = {u: x["state"][u[0], u[1]].cpu().numpy() for u in units}
+    o = torch.empty((B, H_v, D), dtype=torch.bfloat16, device=dev)
+    gdn.gdn_decode(x["q"], x["k"], x["v"], x["g"], x["beta"], x["state"], o)
+    torch.cuda.synchronize()
+
+    def bits(t):
+        return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+    for b, h in units:
+        hq = h * H_qk // H_v
+        o_ref, s_ref = ref.decode(bits(x["q"][b:b + 1, hq:hq + 1]), bits(x["k"][b:b + 1, hq:hq + 1]),
+                                  bits(x["v"][b:b + 1, h:h + 1]), x["g"][b:b + 1, h:h + 1].cpu().numpy(),
+                                  x["beta"][b:b + 1, h:h + 1].cpu().numpy(), before[(b, h)][None, None])
+        check_outputs(bits(o[b:b + 1, h:h + 1]), o_ref, f"decode 8 GiB, unit ({b}, {h})")
+        check_states(x["state"][b:b + 1, h:h + 1].cpu().numpy(), s_ref, f"decode 8 GiB, unit ({b}, {h})")

@@ -170,6 +170,45 @@ def test_prefill_maximum_size():
         check_states(fin[n:n + 1, h:h + 1].cpu().numpy(), s_ref, f"maximum size, unit ({n}, {h})")
 
 
+@pytest.mark.parametrize("L", [10, 4])
+def test_prefill_states_beyond_4gib(L):
+    """4,096 sequences x 32 value heads: 8 GiB of fp32 state in and out, so
+    byte offsets into the states need more than 32 bits past the first half.
+    L = 10: every sequence in the chunk kernel (separate final states); L = 4:
+    every sequence token by token, states in place.  Inputs drawn on the
+    device; the oracle checks the first unit and the one at the highest
+    addresses; the fault word is clear."""
+    import torch
+
+    dev = device()
+    N, H_qk, H_v, D = 4096, 16, 32, 128
+    T = N * L
+    note(f"prefill states beyond 4 GiB: N={N} x {L} tokens, H_v={H_v}")
+    x = wl.prefill_inputs_device(72 + L, N, L, H_qk, H_v, D, 0.02, dev)
+    units = ((0, 0), (N - 1, H_v - 1))
+    before = {u: x["init"][u[0], u[1]].cpu().numpy() for u in units}
+    in_place = L <= 8
+    fin = x["init"] if in_place else torch.empty_like(x["init"])
+    o = torch.empty((T, H_v, D), dtype=torch.bfloat16, device=dev)
+    ws = _workspace(N, T, H_qk, H_v, D, dev)
+    gdn.gdn_prefill_varlen(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], x["init"], fin, o,
+                           workspace=ws)
+    _assert_no_wait_fault(ws, N)
+
+    def bits(t):
+        return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+    for n, h in units:
+        rows = slice(n * L, (n + 1) * L)
+        hq = h * H_qk // H_v
+        o_ref, s_ref = ref.prefill_varlen(
+            bits(x["q"][rows, hq:hq + 1]), bits(x["k"][rows, hq:hq + 1]), bits(x["v"][rows, h:h + 1]),
+            x["g"][rows, h:h + 1].cpu().numpy(), x["beta"][rows, h:h + 1].cpu().numpy(),
+            np.array([0, L], np.int32), before[(n, h)][None, None])
+        check_outputs(bits(o[rows, h:h + 1]), o_ref, f"8 GiB states L={L}, unit ({n}, {h})")
+        check_states(fin[n:n + 1, h:h + 1].cpu().numpy(), s_ref, f"8 GiB states L={L}, unit ({n}, {h})")
+
+
 def test_prefill_identity_gate_bitwise_and_zero_length():
     """g = 0, beta = 0 leaves every state bit for bit; a zero-length sequence
     returns its initial state bit for bit."""
