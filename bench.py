@@ -174,7 +174,7 @@ class MultiToken:
         self.x = _dev_inputs_prefill(self.host, dev)
         self.states = [wl.to_torch(self.host.initial_state, dev) for _ in range(nbuf)]
         self.o = torch.empty((self.T, self.H_v, self.D), dtype=torch.bfloat16, device=dev)
-        ws = gdn.gdn_prefill_workspace_size(self.N, self.T, self.H_qk, self.H_v, self.D, self.D, w["chunk"])
+        ws = gdn.gdn_prefill_workspace_size(self.N, self.T, self.H_v, self.D, self.D, w["chunk"])
         self.ws = torch.empty(max(ws, 256), dtype=torch.uint8, device=dev)
         self.chunk = w["chunk"]
         self.i = 0
@@ -209,7 +209,7 @@ class Prefill:
         self.N, self.T, self.H_qk, self.H_v, self.D, self.C = N, T, H_qk, H_v, D, C
         self.fin = torch.empty((N, H_v, D, D), dtype=torch.float32, device=dev)
         self.o = torch.empty((T, H_v, D), dtype=torch.bfloat16, device=dev)
-        ws = gdn.gdn_prefill_workspace_size(N, T, H_qk, H_v, D, D, C)
+        ws = gdn.gdn_prefill_workspace_size(N, T, H_v, D, D, C)
         self.ws = torch.empty(max(ws, 256), dtype=torch.uint8, device=dev)
         self.flops = prefill_flops(T, H_v, D, C)
         self.bytes = prefill_bytes(T, N, H_qk, H_v, D, state_std is not None)
@@ -222,12 +222,36 @@ class Prefill:
                                self.fin, self.o, chunk=self.C, workspace=self.ws)
 
 
-def _time_parts(parts, steps, warmup):
-    """Run ``warmup`` then ``steps`` steps of all parts in order; per-part HIP
-    event times on torch's current stream (the stream the library launches on)
-    and the wall time of the timed steps.  Returns (ms_per_step, [avg ms per part])."""
+SETTLE = {"seconds": 0.0, "steps": 0}
+
+
+def _settle(parts, seconds):
+    """Untimed steps for about ``seconds`` of wall time before the warm-up:
+    the GPU clocks take about 20 steps of this MFMA-heavy workload to reach
+    their sustained level, so a short --warmup alone would time the ramp.
+    The length is reported in the JSON line (``settle``)."""
     import torch
 
+    n, t0 = 0, time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(5):
+            for p in parts:
+                p()
+        n += 5
+        torch.cuda.synchronize()
+    SETTLE["seconds"] += time.perf_counter() - t0
+    SETTLE["steps"] += n
+
+
+def _time_parts(parts, steps, warmup, settle_s=0.0):
+    """Settle the clocks (``settle_s`` seconds of untimed steps), run
+    ``warmup`` then ``steps`` steps of all parts in order; per-part HIP event
+    times on torch's current stream (the stream the library launches on) and
+    the wall time of the timed steps.  Returns (ms_per_step, [avg ms per part])."""
+    import torch
+
+    if settle_s > 0:
+        _settle(parts, settle_s)
     for _ in range(warmup):
         for p in parts:
             p()
@@ -280,9 +304,23 @@ def _time_graph(fn, launches, replays, warmup):
     return statistics.median(ts) / launches
 
 
+def _host_threads():
+    """(os.cpu_count(), BLAS/OpenMP threads numpy's libraries would use)."""
+    try:
+        from threadpoolctl import threadpool_info
+
+        blas = max((d.get("num_threads", 1) for d in threadpool_info()), default=1)
+    except Exception:  # threadpoolctl missing: report the environment's setting
+        blas = int(os.environ.get("OMP_NUM_THREADS", "1") or 1)
+    return os.cpu_count() or 1, blas
+
+
 def _cpu_baseline_decode(dec, budget_s=10.0):
     """The fp64 oracle's decode (as it stands) timed on the host: repeated full
-    calls on the same batch until about ``budget_s`` of CPU time."""
+    calls on the same batch until about ``budget_s`` of CPU time.  The oracle
+    is vectorised over all (sequence, head) units of the step by numpy; its
+    einsum row dots run on one thread (numpy's einsum does not call BLAS for
+    these shapes), so ``cores`` is 1."""
     import oracle.gdn_ref as ref
 
     h = dec.host
@@ -293,40 +331,52 @@ def _cpu_baseline_decode(dec, budget_s=10.0):
         el = time.perf_counter() - t0
         if el >= budget_s:
             break
-    return dict(value=n * dec.bytes / el / 1e9, unit="GB/s", cores=1, kind="oracle",
+    ncpu, blas = _host_threads()
+    return dict(value=n * dec.bytes / el / 1e9, unit="GB/s", cores=1, host_cpus=ncpu, blas_threads=blas,
+                kind="oracle",
                 sample=f"{n} full decode calls of the timed batch ({dec.B} x {dec.H_v} heads), "
-                       f"{el:.1f} s; numpy fp64 token loop, single-threaded einsum")
+                       f"{el:.1f} s; numpy fp64, vectorised over the units of the step, one thread "
+                       f"(host has {ncpu} CPUs)")
 
 
 def _cpu_baseline_prefill(pre, budget_s=10.0):
-    """The oracle's prefill on a bounded sample: whole (sequence, head) units of
-    the timed batch, one after another, until about ``budget_s``; scaled to
-    tokens/s of all heads (units are independent, so time is linear in units)."""
+    """The oracle's prefill on a bounded sample: whole sequences of the timed
+    batch (all value heads of a sequence advance together, the oracle's token
+    loop vectorised across the independent heads), longest first, until about
+    ``budget_s``; tokens/s = tokens of the sequences done / seconds (units are
+    independent, so time is linear in the sample)."""
+    import numpy as np
     import oracle.gdn_ref as ref
 
     h = pre.host
     cu = h.cu_seqlens
-    unit_tokens, n_units, t0 = 0, 0, time.perf_counter()
+    lens = np.diff(cu)
+    order = sorted(range(pre.N), key=lambda i: -int(lens[i]))
+    tokens, seqs, t0 = 0, 0, time.perf_counter()
     while True:
-        seq = n_units % pre.N
-        head = (7 * n_units) % pre.H_v
-        ref.prefill_units(h.q, h.k, h.v, h.g, h.beta, cu, [(seq, head)], h.initial_state)
-        unit_tokens += int(cu[seq + 1] - cu[seq])
-        n_units += 1
+        n = order[seqs % pre.N]
+        ref.prefill_units(h.q, h.k, h.v, h.g, h.beta, cu, [(n, hh) for hh in range(pre.H_v)],
+                          h.initial_state)
+        tokens += int(lens[n])
+        seqs += 1
         el = time.perf_counter() - t0
         if el >= budget_s:
             break
-    return dict(value=unit_tokens / pre.H_v / el, unit="tokens/s", cores=1, kind="oracle",
-                sample=f"{n_units} (sequence, head) units, {unit_tokens} unit-tokens, {el:.1f} s; "
-                       f"tokens/s = unit-tokens / H_v / seconds")
+    ncpu, blas = _host_threads()
+    return dict(value=tokens / el, unit="tokens/s", cores=1, host_cpus=ncpu, blas_threads=blas,
+                kind="oracle",
+                sample=f"{seqs} whole sequences ({tokens} tokens x {pre.H_v} heads, the heads of a "
+                       f"sequence vectorised in numpy fp64, one thread; host has {ncpu} CPUs), {el:.1f} s")
 
 
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=50,
-                    help="untimed warm-up steps; the clocks settle after about 20 steps of the default workload")
+    ap.add_argument("--warmup", type=int, default=50, help="untimed warm-up steps")
+    ap.add_argument("--settle-s", type=float, default=0.5,
+                    help="seconds of untimed steps before the warm-up, so that the clocks reach their "
+                         "sustained level (about 20 steps of the default workload); reported in the output")
     ap.add_argument("--workload", default="decode_b64+prefill_varlen16",
                     choices=["decode_b64+prefill_varlen16", "decode_b64", "decode_sweep",
                              "prefill_varlen16", "prefill_long2x64k", "decode_multitoken",
@@ -364,6 +414,7 @@ def main(argv=None):
         gbs = 2 * nbytes / (per[0] * 1e-3) / 1e9
         out.update(value=gbs, unit="GB/s", ms_per_step=ms_step, dtype="f32",
                    config=dict(workload="copy_calibration", bytes_read=nbytes, bytes_written=nbytes))
+        out["settle"] = dict(seconds=round(SETTLE["seconds"], 3), steps=SETTLE["steps"])
         print(json.dumps(out), flush=True)
         return 0
 
@@ -390,7 +441,7 @@ def main(argv=None):
     if args.workload == "decode_indexed":
         w = W["decode_b64"]
         di = DecodeIndexed(dev, w["B"], w["H_qk"], w["H_v"], w["D"], w["seed"])
-        ms_step, per = _time_parts([di], args.steps, args.warmup)
+        ms_step, per = _time_parts([di], args.steps, args.warmup, args.settle_s)
         t = per[0] * 1e-3 / di.per_step
         gbs = di.bytes / t / 1e9
         out.update(value=gbs, unit="GB/s", ms_per_step=ms_step, dtype="f32", us_per_launch=t * 1e6,
@@ -399,6 +450,7 @@ def main(argv=None):
                                  kernel="gdn::decode_kernel<128,1,true>", bytes_per_launch=di.bytes),
                    config=dict(workload="decode_indexed", B=di.B, pool_slots=int(di.pool.shape[0]),
                                H_qk=di.H_qk, H_v=di.H_v, d=di.D, launches_per_step=di.per_step))
+        out["settle"] = dict(seconds=round(SETTLE["seconds"], 3), steps=SETTLE["steps"])
         print(json.dumps(out), flush=True)
         return 0
 
@@ -407,8 +459,8 @@ def main(argv=None):
         # the same step through gdn_prefill_varlen (one more launch, which finds
         # nothing to do), timed first, for comparison
         mtp = MultiToken(dev, W["decode_multitoken"], via_prefill=True)
-        _, per_p = _time_parts([mtp], args.steps, args.warmup)
-        ms_step, per = _time_parts([mt], args.steps, args.warmup)
+        _, per_p = _time_parts([mtp], args.steps, args.warmup, args.settle_s)
+        ms_step, per = _time_parts([mt], args.steps, args.warmup, args.settle_s)
         t = per[0] * 1e-3 / mt.per_step
         gbs = mt.bytes / t / 1e9
         out.update(value=gbs, unit="GB/s", ms_per_step=ms_step, dtype="f32",
@@ -423,6 +475,7 @@ def main(argv=None):
                                tokens_per_sequence=mt.Tn,
                                H_qk=mt.H_qk, H_v=mt.H_v, d=mt.D, state_buffers=len(mt.states),
                                launches_per_step=mt.per_step, in_place=True))
+        out["settle"] = dict(seconds=round(SETTLE["seconds"], 3), steps=SETTLE["steps"])
         print(json.dumps(out), flush=True)
         return 0
 
@@ -452,11 +505,12 @@ def main(argv=None):
                                sweep=lines),
                    roofline=dict(bound="hbm", achieved=big["GBs"], peak=HBM_PEAK_GBS, unit="GB/s",
                                  frac=big["frac"], traffic=None))
+        out["settle"] = dict(seconds=round(SETTLE["seconds"], 3), steps=SETTLE["steps"])
         print(json.dumps(out), flush=True)
         return 0
 
     print(f"# bench: timing {args.steps} steps after {args.warmup} warmup", file=sys.stderr, flush=True)
-    ms_step, per = _time_parts(parts, args.steps, args.warmup)
+    ms_step, per = _time_parts(parts, args.steps, args.warmup, args.settle_s)
     times = dict(zip(names, per))
     out["ms_per_step"] = ms_step
     cfg = {}
@@ -496,6 +550,7 @@ def main(argv=None):
                 out["prefill"]["cpu_baseline"] = _cpu_baseline_prefill(pre)
         else:
             out["cpu_baseline"] = _cpu_baseline_prefill(pre)
+    out["settle"] = dict(seconds=round(SETTLE["seconds"], 3), steps=SETTLE["steps"])
     print(json.dumps(out), flush=True)
     return 0
 

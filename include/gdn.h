@@ -116,14 +116,16 @@ GDN_API int gdn_decode_indexed(const void* q, const void* k, const void* v,
                float scale, void* stream);
 
 /*
- * Bytes of device workspace gdn_prefill_varlen needs for N sequences (the
- * longest-first schedule, one int32 per sequence, one int32 count of the
- * sequences run in chunks and one int32 wait-fault word; rounded up to 256
- * bytes).
- * Returns 0 for invalid arguments.
+ * Bytes of device workspace gdn_prefill_varlen (and the other prefill-regime
+ * entry points) needs for N sequences of T tokens in total with H_v value
+ * heads: the longest-first schedule (one int32 per sequence), one int32 count
+ * of the sequences run in chunks and one int32 wait-fault word, rounded up to
+ * 256 bytes.  T, H_v and the head dims enter only through validation today;
+ * they are part of the signature so that the size may depend on them.
+ * Returns 0 for invalid arguments (negative N or T, H_v <= 0, d_k != d_v,
+ * a head dim outside {16, 128} or a chunk other than the one for that dim).
  */
-GDN_API size_t gdn_prefill_workspace_size(int N, int T, int H_qk, int H_v,
-                                  int D_k, int D_v, int chunk);
+GDN_API size_t gdn_prefill_workspace_size(int N, int T, int H_v, int D_k, int D_v, int chunk);
 
 /*
  * gdn_prefill_varlen -- packed variable-length prefill (the prefill regime),
@@ -221,7 +223,7 @@ GDN_API int gdn_prefill_varlen_indexed(const void* q, const void* k, const void*
  *
  *   q, k, v, g, beta, cu_seqlens, o, scale   as gdn_prefill_varlen (D = 128)
  *   state      fp32 [N, H_v, D, D], read and overwritten IN PLACE
- *   workspace  gdn_prefill_workspace_size(N, T, H_qk, H_v, 128, 128, 64)
+ *   workspace  gdn_prefill_workspace_size(N, T, H_v, 128, 128, 64)
  *              bytes, 256-byte aligned.  After the call has completed, bit 1
  *              of int32 word N + 1 is set if some sequence was longer than 8
  *              tokens: such a sequence is skipped (its state and output rows

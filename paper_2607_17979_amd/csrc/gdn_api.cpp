@@ -53,11 +53,20 @@ int chunk_for(int D) { return D == 16 ? 16 : 64; }
 
 }  // namespace
 
+namespace gdn {
+
+size_t prefill_workspace_bytes(int N) {
+    if (N <= 0) return 0;
+    return ((size_t)(N + 2) * sizeof(int32_t) + 255) / 256 * 256;
+}
+
+}  // namespace gdn
+
 extern "C" {
 
 const char* gdn_last_error(void) { return g_last_error.c_str(); }
 
-int gdn_abi_version(void) { return 100; }
+int gdn_abi_version(void) { return 200; }
 
 int gdn_decode(const void* q, const void* k, const void* v, const float* g, const float* beta,
                float* state, void* o, int B, int H_qk, int H_v, int D_k, int D_v, float scale,
@@ -102,25 +111,31 @@ int gdn_decode_indexed(const void* q, const void* k, const void* v, const float*
     return GDN_OK;
 }
 
-size_t gdn_prefill_workspace_size(int N, int T, int H_qk, int H_v, int D_k, int D_v, int chunk) {
-    if (N < 0 || T < 0 || H_qk <= 0 || H_v <= 0 || H_v % H_qk || D_k != D_v ||
-        (D_k != 16 && D_k != 128) || chunk != chunk_for(D_k))
+size_t gdn_prefill_workspace_size(int N, int T, int H_v, int D_k, int D_v, int chunk) {
+    if (N < 0 || T < 0 || H_v <= 0 || D_k != D_v || (D_k != 16 && D_k != 128) || chunk != chunk_for(D_k))
         return 0;
     return gdn::prefill_workspace_bytes(N);
 }
 
-int gdn_prefill_varlen(const void* q, const void* k, const void* v, const float* g,
-                       const float* beta, const int32_t* cu_seqlens, const float* initial_state,
-                       float* final_state, void* o, int N, int T, int H_qk, int H_v, int D_k,
-                       int D_v, int chunk, float scale, void* workspace, size_t workspace_bytes,
-                       void* stream) {
-    g_last_error.clear();
+}  // extern "C"
+
+namespace {
+
+// Checks of gdn_prefill_varlen's arguments other than the workspace; GDN_OK
+// (with *noop set for N = 0) or the failing status with its message.
+int check_prefill(const void* q, const void* k, const void* v, const float* g, const float* beta,
+                  const int32_t* cu_seqlens, const float* initial_state, const float* final_state,
+                  const void* o, int N, int T, int H_qk, int H_v, int D_k, int D_v, int chunk, bool* noop) {
+    *noop = false;
     if (N < 0 || T < 0) return fail(GDN_EINVAL, "N and T must be >= 0 (N=%d, T=%d)", N, T);
     if (int st = check_heads(H_qk, H_v, D_k, D_v)) return st;
     if (chunk != chunk_for(D_k))
         return fail(GDN_EUNSUPPORTED, "chunk %d unsupported for head dim %d (use %d)", chunk, D_k,
                     chunk_for(D_k));
-    if (N == 0) return GDN_OK;
+    if (N == 0) {
+        *noop = true;
+        return GDN_OK;
+    }
     if ((long long)T * H_v > (1LL << 31) / 128 || (long long)N * H_v > (1LL << 30))
         return fail(GDN_EINVAL, "problem too large (N=%d, T=%d, H_v=%d)", N, T, H_v);
     int st;
@@ -140,6 +155,24 @@ int gdn_prefill_varlen(const void* q, const void* k, const void* v, const float*
             (st = check_ptr16(o, "o")) || (st = check_ptr4(g, "g")) || (st = check_ptr4(beta, "beta")))
             return st;
     }
+    return GDN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int gdn_prefill_varlen(const void* q, const void* k, const void* v, const float* g,
+                       const float* beta, const int32_t* cu_seqlens, const float* initial_state,
+                       float* final_state, void* o, int N, int T, int H_qk, int H_v, int D_k,
+                       int D_v, int chunk, float scale, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+    g_last_error.clear();
+    bool noop;
+    if (int st = check_prefill(q, k, v, g, beta, cu_seqlens, initial_state, final_state, o, N, T, H_qk, H_v,
+                               D_k, D_v, chunk, &noop))
+        return st;
+    if (noop) return GDN_OK;
     const size_t need = gdn::prefill_workspace_bytes(N);
     if (workspace == nullptr || workspace_bytes < need)
         return fail(GDN_EWORKSPACE, "workspace of %zu bytes needed, %zu given%s", need,

@@ -1,0 +1,129 @@
+// Index arithmetic of the kernels' work walks: which workgroup takes which
+// (sequence, value head, column or row block) item, and the fields of an
+// item.  Plain integer functions, compiled for the host as well as the
+// device, so that a host build (with the address and undefined-behaviour
+// sanitizers) can enumerate every walk and compare it with an independent
+// enumeration.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gdn {
+
+constexpr int kSortMax = 4096;  // larger batches keep their given order
+
+// blockIdx -> logical work index.  The P consecutive work items P j .. P j +
+// P - 1 (items that read the same q/k rows: the two value heads of a q/k head,
+// times the value-column blocks of each) go to workgroups 8 apart, which the
+// dispatcher places on the same XCD, so their reads share that L2.  A last
+// partial group of 8 P items keeps the identity mapping.  A bijection of
+// [0, total).
+template <int P = 2>
+__host__ __device__ inline int logical_item(int bid, int total) {
+    constexpr int G = 8 * P;
+    const int grp = bid / G;
+    if (grp * G + G > total) return bid;
+    const int r = bid - grp * G;
+    return grp * G + P * (r & 7) + (r >> 3);
+}
+
+// Rank of sequence i when sequences are ordered by decreasing length, ties by
+// index (len: the N lengths).
+__host__ __device__ inline int longest_first_rank(const int* len, int N, int i) {
+    const int li = len[i];
+    int rank = 0;
+    for (int j = 0; j < N; ++j) {
+        const int lj = len[j];
+        rank += (lj > li) || (lj == li && j < i);
+    }
+    return rank;
+}
+
+// ---- token-by-token kernel: units (sequence n, value head h, row block blk),
+// u = (n H_v + h) BPH + blk, walked by workgroup w (w >= 1) as w - 1,
+// w - 1 + stride, ...
+
+// Whether unit u runs in the token-by-token kernel: its sequence has at most
+// recur_max tokens and its state lies inside the pool (with state_idx).
+__host__ __device__ inline bool recur_unit_runs(long u, int bph, int H_v, const int32_t* cu,
+                                                const int32_t* state_idx, int P, int recur_max) {
+    const int n = (int)(u / bph / H_v);
+    if (cu[n + 1] - cu[n] > recur_max) return false;
+    if (state_idx != nullptr) {
+        const int slot = state_idx[n];
+        if (slot < 0 || slot >= P) return false;
+    }
+    return true;
+}
+
+// The first unit at or after u (stepping by stride) that runs here, or a
+// value >= units.
+__host__ __device__ inline long recur_next_unit(long u, long stride, long units, int bph, int H_v,
+                                                const int32_t* cu, const int32_t* state_idx, int P,
+                                                int recur_max) {
+    while (u < units && !recur_unit_runs(u, bph, H_v, cu, state_idx, P, recur_max)) u += stride;
+    return u;
+}
+
+// Fields of a unit that runs: its head, q/k head, row block, tokens and state
+// (state n H_v + h, or pool slot state_idx[n] H_v + h).
+struct RecurUnit {
+    long u, shead;
+    int h, hq, blk, t0, len;
+};
+__host__ __device__ inline RecurUnit recur_unit_at(long u, int bph, int H_v, int H_qk, const int32_t* cu,
+                                                   const int32_t* state_idx) {
+    RecurUnit r;
+    const long head = u / bph;  // n H_v + h
+    const int n = (int)(head / H_v);
+    r.u = u;
+    r.h = (int)(head - (long)n * H_v);
+    r.hq = r.h / (H_v / H_qk);
+    r.blk = (int)(u - head * bph);
+    r.t0 = cu[n];
+    r.len = cu[n + 1] - r.t0;
+    r.shead = state_idx != nullptr ? (long)state_idx[n] * H_v + r.h : head;
+    return r;
+}
+
+// ---- chunk kernel: items (rank, value head h, value block vb), item =
+// (rank H_v + h) VSPLIT + vb, over G workgroups: on pass p workgroup b takes
+// the virtual index p G + b (p even) or p G + G - 1 - b (p odd), mapped by
+// logical_item<2 VSPLIT>; -1 past the last item.
+template <int VSPLIT>
+__host__ __device__ inline int pipe_item_at(int pass, int G, int bid, int items) {
+    const int vb = pass * G + ((pass & 1) ? G - 1 - bid : bid);
+    return vb < items ? logical_item<2 * VSPLIT>(vb, items) : -1;
+}
+
+// Fields of a chunk-kernel item: sequence (order[rank]), value head, q/k head,
+// value block, tokens, chunk count (0: not the chunk kernel's, or outside the
+// pool) and state (sequence n, or its pool slot).
+struct PipeItem {
+    int n, h, hq, vblock, seq_beg, seq_len, nch;
+    long slot;
+};
+__host__ __device__ inline PipeItem pipe_item_fields(int item, int vsplit, int H_v, int H_qk,
+                                                     const int32_t* order, const int32_t* cu,
+                                                     const int32_t* state_idx, int P, int chunk,
+                                                     int recur_max) {
+    PipeItem it;
+    const int head_item = item / vsplit;
+    it.vblock = item - head_item * vsplit;
+    const int rank = head_item / H_v;
+    it.h = head_item - rank * H_v;
+    it.n = order[rank];
+    it.hq = it.h / (H_v / H_qk);
+    it.seq_beg = cu[it.n];
+    it.seq_len = cu[it.n + 1] - it.seq_beg;
+    it.nch = it.seq_len <= recur_max ? 0 : (it.seq_len + chunk - 1) / chunk;
+    it.slot = it.n;
+    if (state_idx != nullptr) {
+        it.slot = state_idx[it.n];
+        if (it.slot < 0 || it.slot >= P) it.nch = 0;
+    }
+    return it;
+}
+
+}  // namespace gdn

@@ -9,6 +9,7 @@
 #pragma once
 
 #include "gdn_device.h"
+#include "gdn_index.h"
 
 namespace gdn {
 
@@ -150,20 +151,6 @@ __device__ __forceinline__ typename Frag<K>::type acc_frag_hi(const f32x4_t& t0,
 __device__ __forceinline__ void split_bf16(float x, uint16_t& hi, uint16_t& lo) {
     hi = f32_to_bf16(x);
     lo = f32_to_bf16(x - bf16_to_f32(hi));
-}
-
-// blockIdx -> logical work index.  The P consecutive work items P j .. P j +
-// P - 1 (items that read the same q/k rows: the two value heads of a q/k head,
-// times the value-column blocks of each) go to workgroups 8 apart, which the
-// dispatcher places on the same XCD, so their reads share that L2.  A last
-// partial group of 8 P items keeps the identity mapping.
-template <int P = 2>
-__device__ __forceinline__ int logical_item(int bid, int total) {
-    constexpr int G = 8 * P;
-    const int grp = bid / G;
-    if (grp * G + G > total) return bid;
-    const int r = bid - grp * G;
-    return grp * G + P * (r & 7) + (r >> 3);
 }
 
 }  // namespace gdn

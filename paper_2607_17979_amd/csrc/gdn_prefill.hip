@@ -479,10 +479,6 @@ __global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
         }
 }
 
-size_t prefill_workspace_bytes(int N) {
-    if (N <= 0) return 0;
-    return ((size_t)(N + 2) * sizeof(int32_t) + 255) / 256 * 256;
-}
 
 hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {
     int32_t* order = static_cast<int32_t*>(a.workspace);

@@ -536,32 +536,10 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
     const int items = N * H_v * VSPLIT;
     const int G = gridDim.x;
     const int bid = blockIdx.x;
-    auto item_at = [&](int pass) -> int {
-        const int vb = pass * G + ((pass & 1) ? G - 1 - bid : bid);
-        return vb < items ? logical_item<2 * VSPLIT>(vb, items) : -1;
-    };
-    struct Item {
-        int n, h, hq, vblock, seq_beg, seq_len, nch;
-        long slot;  // state of the sequence: state n or a pool slot
-    };
+    auto item_at = [&](int pass) -> int { return pipe_item_at<VSPLIT>(pass, G, bid, items); };
+    typedef PipeItem Item;
     auto decode = [&](int item) -> Item {
-        Item it;
-        const int head_item = item / VSPLIT;
-        it.vblock = item - head_item * VSPLIT;
-        const int rank = head_item / H_v;
-        it.h = head_item - rank * H_v;
-        it.n = order[rank];
-        it.hq = it.h / (H_v / H_qk);
-        it.seq_beg = cu[it.n];
-        it.seq_len = cu[it.n + 1] - it.seq_beg;
-        // sequences of at most kRecurMax tokens belong to the recurrent kernel
-        it.nch = it.seq_len <= kRecurMax ? 0 : (it.seq_len + C - 1) / C;
-        it.slot = it.n;
-        if (state_idx != nullptr) {
-            it.slot = state_idx[it.n];
-            if (it.slot < 0 || it.slot >= P) it.nch = 0;  // outside the pool: skipped
-        }
-        return it;
+        return pipe_item_fields(item, VSPLIT, H_v, H_qk, order, cu, state_idx, P, C, kRecurMax);
     };
     const size_t qk_stride = (size_t)H_qk * D;
     const size_t v_stride = (size_t)H_v * D;

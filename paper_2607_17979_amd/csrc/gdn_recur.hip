@@ -28,6 +28,7 @@
 #include <algorithm>
 
 #include "gdn_device.h"
+#include "gdn_index.h"
 #include "gdn_launch.h"
 #include "gdn_schedule.h"
 
@@ -91,38 +92,13 @@ __global__ __launch_bounds__(256) void prefill_recur_kernel(
     // Unit u runs here if its sequence has at most kRecurMax tokens and its
     // state lies inside the pool; a workgroup walks units u, u + stride, ...
     const long stride = gridDim.x - 1;
-    auto runs_here = [&](long u) -> bool {
-        const int n = (int)(u / BPH / H_v);
-        if (cu[n + 1] - cu[n] > kRecurMax) return false;  // the chunk kernel's
-        if (state_idx != nullptr) {
-            const int slot = state_idx[n];
-            if (slot < 0 || slot >= P) return false;  // outside the pool: skipped
-        }
-        return true;
-    };
     auto next_unit = [&](long u) -> long {
-        while (u < units && !runs_here(u)) u += stride;
-        return u;
+        return recur_next_unit(u, stride, units, BPH, H_v, cu, state_idx, P, kRecurMax);
     };
     // The fields of a unit that runs here: its state (state n, or pool slot
     // state_idx[n]), head, row block and tokens.
-    struct Unit {
-        long u, shead;
-        int h, hq, blk, t0, len;
-    };
-    auto unit_at = [&](long u) -> Unit {
-        Unit r;
-        const long head = u / BPH;  // n H_v + h
-        const int n = (int)(head / H_v);
-        r.u = u;
-        r.h = (int)(head - (long)n * H_v);
-        r.hq = r.h / (H_v / H_qk);
-        r.blk = (int)(u - head * BPH);
-        r.t0 = cu[n];
-        r.len = cu[n + 1] - r.t0;
-        r.shead = state_idx != nullptr ? (long)state_idx[n] * H_v + r.h : head;
-        return r;
-    };
+    typedef RecurUnit Unit;
+    auto unit_at = [&](long u) -> Unit { return recur_unit_at(u, BPH, H_v, H_qk, cu, state_idx); };
     auto state_row = [&](const Unit& x) {
         const int row = x.blk * ROWS + wave * ROWS_PER_WAVE + sub;
         return ((size_t)x.shead * D + row) * D;

@@ -6,9 +6,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-namespace gdn {
+#include "gdn_index.h"
 
-constexpr int kSortMax = 4096;  // larger batches keep their given order
+namespace gdn {
 
 // Run by one whole workgroup: order[rank] = sequence index, ranks by decreasing
 // length with ties by index.  len: kSortMax ints of LDS.
@@ -20,15 +20,7 @@ __device__ __forceinline__ void schedule_longest_first(const int32_t* __restrict
     }
     for (int i = threadIdx.x; i < N; i += blockDim.x) len[i] = cu[i + 1] - cu[i];
     __syncthreads();
-    for (int i = threadIdx.x; i < N; i += blockDim.x) {
-        const int li = len[i];
-        int rank = 0;
-        for (int j = 0; j < N; ++j) {
-            const int lj = len[j];
-            rank += (lj > li) || (lj == li && j < i);
-        }
-        order[rank] = i;
-    }
+    for (int i = threadIdx.x; i < N; i += blockDim.x) order[longest_first_rank(len, N, i)] = i;
 }
 
 }  // namespace gdn

@@ -25,6 +25,7 @@ __all__ = [
     "gdn_prefill_varlen",
     "gdn_prefill_varlen_indexed",
     "gdn_decode_multitoken",
+    "workspace_fault",
     "EXPORTED_SYMBOLS",
 ]
 
@@ -67,7 +68,7 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.gdn_decode_indexed.restype = ci
     lib.gdn_decode_indexed.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, cf, vp]
     lib.gdn_prefill_workspace_size.restype = sz
-    lib.gdn_prefill_workspace_size.argtypes = [ci, ci, ci, ci, ci, ci, ci]
+    lib.gdn_prefill_workspace_size.argtypes = [ci, ci, ci, ci, ci, ci]
     lib.gdn_prefill_varlen.restype = ci
     lib.gdn_prefill_varlen.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                        ci, ci, ci, ci, ci, ci, ci, cf, vp, sz, vp]
@@ -105,6 +106,41 @@ def _stream(t, stream) -> Optional[int]:
     if stream is None:
         stream = torch.cuda.current_stream(t.device)
     return getattr(stream, "cuda_stream", stream)
+
+
+def _torch_stream(t, stream):
+    """The launch stream as a torch stream object (a raw hipStream_t handle is
+    wrapped, not adopted)."""
+    import torch
+
+    if stream is None:
+        return torch.cuda.current_stream(t.device)
+    if isinstance(stream, torch.cuda.Stream):
+        return stream
+    return torch.cuda.ExternalStream(int(stream), device=t.device)
+
+
+def _workspace_for(t, need, workspace, stream):
+    """The caller's workspace, or a new one allocated on the launch stream, so
+    that torch's caching allocator does not hand its memory to other work
+    while the kernels of this call may still use it."""
+    import torch
+
+    if workspace is not None:
+        return workspace
+    with torch.cuda.stream(_torch_stream(t, stream)):
+        return torch.empty(max(need, 256), dtype=torch.uint8, device=t.device)
+
+
+def workspace_fault(workspace, N: int) -> int:
+    """The wait-fault word of a prefill workspace after the call that used it
+    has completed (synchronises the device): 0, or bit 0 set if a wave of the
+    chunk kernel gave up a bounded wait (results invalid), bit 1 set if
+    gdn_decode_multitoken met a sequence longer than 8 tokens."""
+    import torch
+
+    torch.cuda.synchronize(workspace.device)
+    return int(workspace.view(torch.int32)[N + 1].item())
 
 
 def _need(t, name, dtype, shape, device):
@@ -173,9 +209,8 @@ def gdn_decode_indexed(q, k, v, g, beta, state_pool, state_idx, o, scale: float 
                                   _stream(q, stream)))
 
 
-def gdn_prefill_workspace_size(N: int, T: int, H_qk: int, H_v: int, D_k: int, D_v: int,
-                               chunk: int) -> int:
-    return int(load_library().gdn_prefill_workspace_size(N, T, H_qk, H_v, D_k, D_v, chunk))
+def gdn_prefill_workspace_size(N: int, T: int, H_v: int, D_k: int, D_v: int, chunk: int) -> int:
+    return int(load_library().gdn_prefill_workspace_size(N, T, H_v, D_k, D_v, chunk))
 
 
 def default_chunk(D: int) -> int:
@@ -184,13 +219,14 @@ def default_chunk(D: int) -> int:
 
 def gdn_prefill_varlen(q, k, v, g, beta, cu_seqlens, initial_state, final_state, o,
                        scale: float = 1.0, chunk: Optional[int] = None, workspace=None,
-                       stream=None) -> None:
+                       stream=None):
     """Packed varlen prefill (see include/gdn.h).  q, k: bf16 [T, H_qk, D]; v:
     bf16 [T, H_v, D]; g, beta: fp32 [T, H_v]; cu_seqlens: int32 [N + 1] on the
     device; initial_state: fp32 [N, H_v, D, D] or None; final_state: fp32
     [N, H_v, D, D] (may be initial_state); o: bf16 [T, H_v, D].  ``workspace``
     (uint8, at least gdn_prefill_workspace_size bytes) is allocated with torch
-    when omitted."""
+    when omitted, on the launch stream.  Returns the workspace (its int32 word
+    N + 1 is the wait-fault word, see ``workspace_fault``)."""
     import torch
 
     T, H_qk, D = q.shape
@@ -210,20 +246,20 @@ def gdn_prefill_varlen(q, k, v, g, beta, cu_seqlens, initial_state, final_state,
     _need(final_state, "final_state", torch.float32, (N, H_v, D, D), dev)
     _need(o, "o", torch.bfloat16, (T, H_v, D), dev)
     chunk = default_chunk(D) if chunk is None else chunk
-    need = gdn_prefill_workspace_size(N, T, H_qk, H_v, D, D, chunk)
-    if workspace is None:
-        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    need = gdn_prefill_workspace_size(N, T, H_v, D, D, chunk)
+    workspace = _workspace_for(q, need, workspace, stream)
     lib = load_library()
     _check(lib.gdn_prefill_varlen(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
                                   _ptr(cu_seqlens), _ptr(initial_state), _ptr(final_state),
                                   _ptr(o), N, T, H_qk, H_v, D, D, chunk, float(scale),
                                   _ptr(workspace), workspace.numel() * workspace.element_size(),
                                   _stream(q, stream)))
+    return workspace
 
 
 def gdn_prefill_varlen_indexed(q, k, v, g, beta, cu_seqlens, state_pool, state_idx, o,
                                scale: float = 1.0, chunk: Optional[int] = None, workspace=None,
-                               stream=None) -> None:
+                               stream=None):
     """Packed varlen prefill on pooled states (see include/gdn.h).  As
     gdn_prefill_varlen, with state_pool: fp32 [P, H_v, D, D] (sequence n starts
     from slot state_idx[n] and leaves its final state there) and state_idx:
@@ -247,24 +283,25 @@ def gdn_prefill_varlen_indexed(q, k, v, g, beta, cu_seqlens, state_pool, state_i
     _need(state_idx, "state_idx", torch.int32, (N,), dev)
     _need(o, "o", torch.bfloat16, (T, H_v, D), dev)
     chunk = default_chunk(D) if chunk is None else chunk
-    need = gdn_prefill_workspace_size(N, T, H_qk, H_v, D, D, chunk)
-    if workspace is None:
-        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    need = gdn_prefill_workspace_size(N, T, H_v, D, D, chunk)
+    workspace = _workspace_for(q, need, workspace, stream)
     lib = load_library()
     _check(lib.gdn_prefill_varlen_indexed(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
                                           _ptr(cu_seqlens), _ptr(state_pool), _ptr(state_idx),
                                           _ptr(o), N, T, P, H_qk, H_v, D, D, chunk, float(scale),
                                           _ptr(workspace), workspace.numel() * workspace.element_size(),
                                           _stream(q, stream)))
+    return workspace
 
 
 def gdn_decode_multitoken(q, k, v, g, beta, cu_seqlens, state, o, scale: float = 1.0,
-                          workspace=None, stream=None) -> None:
+                          workspace=None, stream=None):
     """Decode step of at most 8 new tokens per sequence, state in place (see
     include/gdn.h).  q, k: bf16 [T, H_qk, 128]; v: bf16 [T, H_v, 128]; g, beta:
     fp32 [T, H_v]; cu_seqlens: int32 [N + 1] on the device; state: fp32
     [N, H_v, 128, 128]; o: bf16 [T, H_v, 128].  ``workspace`` (uint8, at least
-    gdn_prefill_workspace_size bytes) is allocated with torch when omitted."""
+    gdn_prefill_workspace_size bytes) is allocated with torch on the launch
+    stream when omitted.  Returns the workspace."""
     import torch
 
     T, H_qk, D = q.shape
@@ -281,11 +318,12 @@ def gdn_decode_multitoken(q, k, v, g, beta, cu_seqlens, state, o, scale: float =
     _need(cu_seqlens, "cu_seqlens", torch.int32, (N + 1,), dev)
     _need(state, "state", torch.float32, (N, H_v, D, D), dev)
     _need(o, "o", torch.bfloat16, (T, H_v, D), dev)
-    need = gdn_prefill_workspace_size(N, T, H_qk, H_v, D, D, default_chunk(D))
-    if workspace is None:
-        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    need = gdn_prefill_workspace_size(N, T, H_v, D, D, default_chunk(D))
+    workspace = _workspace_for(q, need, workspace, stream)
     lib = load_library()
     _check(lib.gdn_decode_multitoken(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(cu_seqlens),
                                      _ptr(state), _ptr(o), N, T, H_qk, H_v, D, D, float(scale),
                                      _ptr(workspace), workspace.numel() * workspace.element_size(),
                                      _stream(q, stream)))
+    return workspace
+

@@ -201,13 +201,16 @@ def prefill_inputs(seed: int, lengths: Sequence[int], H_qk: int, H_v: int, D: in
 
 
 def prefill_inputs_device(seed: int, N: int, L: int, H_qk: int, H_v: int, D: int,
-                          state_std: float, device):
+                          state_std: float, device, g_scale: float = 1.0,
+                          beta_range: Optional[Tuple[float, float]] = None):
     """An equal-length packed batch (N sequences of L tokens) drawn on the GPU
     with torch's seeded generator, for sizes whose host draw would take
     minutes; the same distributions as prefill_inputs: q, k N(0, 1)
     L2-normalised per head in fp32, then rounded to bf16; v N(0, 1) in bf16;
     beta = sigmoid(N(0, 1)); g = -softplus(N(0, 1)); initial state
-    N(0, state_std^2).  Returns a dict of device tensors (q, k, v, g, beta,
+    N(0, state_std^2).  ``g_scale`` multiplies g (0 gives g = 0 exactly, slow
+    decay regimes lie between); ``beta_range`` = (lo, hi) draws beta uniformly
+    in [lo, hi) instead.  Returns a dict of device tensors (q, k, v, g, beta,
     init, cu)."""
     import torch
 
@@ -228,7 +231,11 @@ def prefill_inputs_device(seed: int, N: int, L: int, H_qk: int, H_v: int, D: int
                 x = x / x.norm(dim=-1, keepdim=True)
             dst[t0:t0 + L] = x.to(torch.bfloat16)
     beta = torch.sigmoid(normal((T, H_v)))
+    if beta_range is not None:
+        u = torch.rand((T, H_v), generator=gen, device=device, dtype=torch.float32)
+        beta = beta_range[0] + (beta_range[1] - beta_range[0]) * u
     g = -torch.nn.functional.softplus(normal((T, H_v)))
+    g = g * g_scale if g_scale != 0.0 else torch.zeros_like(g)
     init = torch.empty((N, H_v, D, D), dtype=torch.float32, device=device)
     for n0 in range(0, N, 256):  # in slices: no second full-size temporary
         init[n0:n0 + 256] = state_std * normal((min(256, N - n0), H_v, D, D))

@@ -1,0 +1,106 @@
+// Host-only enumeration of the kernels' work walks for the sanitizer build:
+// the token-by-token kernel's unit walk (as the kernel runs it, and a
+// reconstruction of an earlier form that scanned for the next unit and
+// returned every field of it from one function), the longest-first schedule
+// and the chunk kernel's item walk, all through the functions the kernels
+// call (gdn_index.h).  Reads a configuration from stdin, prints one line per
+// visited unit or item; the test compares them with its own enumeration.
+#include <cstdio>
+#include <iostream>
+#include <vector>
+
+#include "gdn_index.h"
+
+using namespace gdn;
+
+namespace {
+
+constexpr int kRecurMax = 8;  // sequences of at most this many tokens run token by token
+constexpr int kBph = 4;       // workgroups (row blocks) per (sequence, head) in that kernel
+constexpr int kChunk = 64;
+
+// The earlier form of the walk, reconstructed: one function scans for the
+// next unit that runs and returns all of its fields.
+RecurUnit legacy_next(long u, long stride, long units, int H_v, int H_qk, const int32_t* cu,
+                      const int32_t* state_idx, int P) {
+    RecurUnit r;
+    for (; u < units; u += stride) {
+        const long head = u / kBph;
+        const int n = (int)(head / H_v);
+        r.h = (int)(head - (long)n * H_v);
+        r.t0 = cu[n];
+        r.len = cu[n + 1] - r.t0;
+        if (r.len > kRecurMax) continue;
+        long shead = head;
+        if (state_idx != nullptr) {
+            const long slot = state_idx[n];
+            if (slot < 0 || slot >= P) continue;
+            shead = slot * H_v + r.h;
+        }
+        r.u = u;
+        r.hq = r.h / (H_v / H_qk);
+        r.blk = (int)(u - head * kBph);
+        r.shead = shead;
+        return r;
+    }
+    r = RecurUnit{units, 0, 0, 0, 0, 0, 0};
+    return r;
+}
+
+template <int VSPLIT>
+void pipe_walk(int G, int items, int H_v, int H_qk, const int32_t* order, const int32_t* cu,
+               const int32_t* state_idx, int P) {
+    for (int b = 0; b < G; ++b)
+        for (int pass = 0;; ++pass) {
+            const int item = pipe_item_at<VSPLIT>(pass, G, b, items);
+            if (item < 0) break;
+            const PipeItem it = pipe_item_fields(item, VSPLIT, H_v, H_qk, order, cu, state_idx, P, kChunk, kRecurMax);
+            std::printf("pipe %d %d %d %d %d %d %d %ld %d %d\n", b, pass, item, it.n, it.h, it.vblock, it.nch,
+                        it.slot, it.seq_beg, it.seq_len);
+        }
+}
+
+}  // namespace
+
+int main() {
+    int N, H_qk, H_v, P, grid_recur, grid_pipe, vsplit, use_idx;
+    std::cin >> N >> H_qk >> H_v >> P >> grid_recur >> grid_pipe >> vsplit >> use_idx;
+    std::vector<int32_t> len(N), cu(N + 1, 0), idx(N, 0);
+    for (int i = 0; i < N; ++i) {
+        std::cin >> len[i];
+        cu[i + 1] = cu[i] + len[i];
+    }
+    if (use_idx)
+        for (int i = 0; i < N; ++i) std::cin >> idx[i];
+    const int32_t* sidx = use_idx ? idx.data() : nullptr;
+    // token-by-token walk, as the kernel runs it: workgroups 1 .. grid - 1
+    const long units = (long)N * H_v * kBph, stride = grid_recur - 1;
+    for (int b = 1; b < grid_recur; ++b) {
+        long u = recur_next_unit(b - 1, stride, units, kBph, H_v, cu.data(), sidx, P, kRecurMax);
+        while (u < units) {
+            const RecurUnit r = recur_unit_at(u, kBph, H_v, H_qk, cu.data(), sidx);
+            std::printf("recur %d %ld %d %d %d %ld %d %d\n", b, r.u, r.h, r.hq, r.blk, r.shead, r.t0, r.len);
+            u = recur_next_unit(u + stride, stride, units, kBph, H_v, cu.data(), sidx, P, kRecurMax);
+        }
+        for (RecurUnit r = legacy_next(b - 1, stride, units, H_v, H_qk, cu.data(), sidx, P); r.u < units;
+             r = legacy_next(r.u + stride, stride, units, H_v, H_qk, cu.data(), sidx, P))
+            std::printf("legacy %d %ld %d %d %d %ld %d %d\n", b, r.u, r.h, r.hq, r.blk, r.shead, r.t0, r.len);
+    }
+    // longest-first schedule (identity beyond kSortMax sequences)
+    std::vector<int32_t> order(N);
+    for (int i = 0; i < N; ++i) order[N > kSortMax ? i : longest_first_rank(len.data(), N, i)] = i;
+    for (int r = 0; r < N; ++r) std::printf("order %d %d\n", r, order[r]);
+    // chunk-kernel item walk
+    const int items = N * H_v * vsplit;
+    if (vsplit == 1) pipe_walk<1>(grid_pipe, items, H_v, H_qk, order.data(), cu.data(), sidx, P);
+    if (vsplit == 2) pipe_walk<2>(grid_pipe, items, H_v, H_qk, order.data(), cu.data(), sidx, P);
+    if (vsplit == 4) pipe_walk<4>(grid_pipe, items, H_v, H_qk, order.data(), cu.data(), sidx, P);
+    // logical_item: bijections
+    for (int total : {1, 7, 16, 31, 32, 33, 100, 257}) {
+        for (int bid = 0; bid < total; ++bid)
+            std::printf("logical2 %d %d %d\n", total, bid, logical_item<2>(bid, total));
+        for (int bid = 0; bid < total; ++bid)
+            std::printf("logical8 %d %d %d\n", total, bid, logical_item<8>(bid, total));
+    }
+    return 0;
+}

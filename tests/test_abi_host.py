@@ -42,7 +42,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert lib.gdn_abi_version() == 100
+    assert lib.gdn_abi_version() == 200
 
 
 def decode(lib, q=P, k=P, v=P, g=P, beta=P, state=P, o=P, B=2, H_qk=1, H_v=2, Dk=128, Dv=128,
@@ -72,18 +72,22 @@ def test_decode_zero_batch_is_noop(lib):
     assert gdn.gdn_last_error() == ""
 
 
-def ws_size(lib, N=3, T=10, H_qk=1, H_v=2, D=128, chunk=64):
-    return lib.gdn_prefill_workspace_size(N, T, H_qk, H_v, D, D, chunk)
+def ws_size(lib, N=3, T=10, H_v=2, D=128, chunk=64, Dv=None):
+    return lib.gdn_prefill_workspace_size(N, T, H_v, D, D if Dv is None else Dv, chunk)
 
 
 def test_workspace_size(lib):
+    """The signature is (N, T, H_v, D_k, D_v, chunk): the schedule, the
+    chunk-kernel count and the fault word, rounded up to 256 bytes."""
     assert ws_size(lib) == 256
     assert ws_size(lib, N=100) == 512
     assert ws_size(lib, N=0) == 0
     assert ws_size(lib, D=16, chunk=16) == 256
     assert ws_size(lib, chunk=16) == 0
-    assert ws_size(lib, H_qk=3, H_v=4) == 0
+    assert ws_size(lib, H_v=0) == 0
+    assert ws_size(lib, D=128, Dv=16) == 0
     assert ws_size(lib, N=-1) == 0
+    assert ws_size(lib, T=-1) == 0
 
 
 def decode_indexed(lib, q=P, k=P, v=P, g=P, beta=P, pool=P, idx=P, o=P, B=2, Pn=4, H_qk=1, H_v=2,
@@ -223,3 +227,4 @@ def test_decode_multitoken_rejects(lib, kw, status, msg):
 def test_decode_multitoken_empty_is_noop(lib):
     assert multitoken(lib, q=None, k=None, v=None, g=None, beta=None, cu=None, state=None, o=None,
                       N=0, T=0, ws=None, ws_bytes=0) == OK
+

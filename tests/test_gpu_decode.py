@@ -25,7 +25,7 @@ def test_library_is_the_native_one():
 
     dev = device()
     lib = gdn.load_library()
-    assert lib.gdn_abi_version() == 100
+    assert lib.gdn_abi_version() == 200
     maps = open("/proc/self/maps").read()
     assert "libgdn_mi355x.so" in maps
     assert torch.cuda.get_device_properties(dev).gcnArchName.startswith("gfx950")
@@ -76,24 +76,27 @@ def _sample_units(rng, B, H_v, n):
     return flat // H_v, flat % H_v
 
 
+@pytest.mark.parametrize("seed_off", [0, 1000, 2000])
 @pytest.mark.parametrize("B", [1, 8, 256, 1024])
-def test_decode_sweep_100_steps(B):
-    """100 consecutive in-place steps with fresh inputs; the oracle follows a
-    seeded sample of (b, h) units (units are independent, so this is exact)."""
+def test_decode_sweep_100_steps(B, seed_off):
+    """100 consecutive in-place steps with fresh inputs, three seeds per batch
+    size; the oracle follows a seeded sample of (b, h) units (units are
+    independent, so this is exact)."""
     import torch
 
     dev = device()
     w = wl.WORKLOADS["decode_sweep"]
     H_qk, H_v, D, steps = w["H_qk"], w["H_v"], w["D"], w["steps"]
-    note(f"decode sweep B={B} x {steps} steps")
-    state0 = wl.decode_state(w["seed"] + B, B, H_v, D, w["state_std"])
+    seed = w["seed"] + B + seed_off
+    note(f"decode sweep B={B} x {steps} steps, seed {seed}")
+    state0 = wl.decode_state(seed, B, H_v, D, w["state_std"])
     state = to_dev(state0, dev)
-    bs, hs = _sample_units(np.random.default_rng(B), B, H_v, 32)
+    bs, hs = _sample_units(np.random.default_rng(B + seed_off), B, H_v, 32)
     hq = ref.head_map(H_qk, H_v)
     S = ref.to_f64(state0[bs, hs])[:, None]
     worst_o = 0.0
     for s in range(steps):
-        st = wl.decode_step_inputs(w["seed"] + B, s, B, H_qk, H_v, D)
+        st = wl.decode_step_inputs(seed, s, B, H_qk, H_v, D)
         o = _decode_gpu(st, state, dev)
         o_ref, S = ref.decode(st.q[bs, hq[hs]][:, None], st.k[bs, hq[hs]][:, None],
                               st.v[bs, hs][:, None], st.g[bs, hs][:, None], st.beta[bs, hs][:, None], S)

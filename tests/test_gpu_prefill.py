@@ -15,7 +15,7 @@ def _workspace(N, T, H_qk, H_v, D, dev):
     reads 0 afterwards only if the call cleared it."""
     import torch
 
-    need = gdn.gdn_prefill_workspace_size(N, T, H_qk, H_v, D, D, gdn.default_chunk(D))
+    need = gdn.gdn_prefill_workspace_size(N, T, H_v, D, D, gdn.default_chunk(D))
     return torch.full((max(need, 256),), 255, dtype=torch.uint8, device=dev)
 
 
