@@ -181,6 +181,30 @@ GDN_API int gdn_prefill_varlen(const void* q, const void* k, const void* v,
                        void* stream);
 
 /*
+ * gdn_prefill_varlen_noalloc -- gdn_prefill_varlen for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the same arguments without the
+ * workspace, and the same kernels and results bit for bit.  The workspace is
+ * a static device array of the library (one copy per GPU, about 64 KiB, held
+ * until the process ends), so N is limited to 16,384 sequences (GDN_EWORKSPACE
+ * beyond that, before any HIP call).  The call allocates and frees nothing;
+ * its first call on a device looks up the array's address there (no
+ * allocation).  Every call on one GPU shares that array and each call's first
+ * launch rewrites what it needs, so calls that overlap in time on one GPU
+ * (concurrent streams, or host threads) race and must not be issued; calls
+ * one after another on a stream are fine.  The wait-fault word of the
+ * workspace is not reported by this entry point.  Other errors as
+ * gdn_prefill_varlen.
+ */
+GDN_API int gdn_prefill_varlen_noalloc(const void* q, const void* k, const void* v,
+                       const float* g, const float* beta,
+                       const int32_t* cu_seqlens,
+                       const float* initial_state, float* final_state,
+                       void* o,
+                       int N, int T, int H_qk, int H_v, int D_k, int D_v,
+                       int chunk, float scale, void* stream);
+
+/*
  * gdn_prefill_varlen_indexed -- gdn_prefill_varlen on states kept in a pool
  * of P slots: sequence n starts from slot state_idx[n] and leaves its final
  * state there (in place).  Serving code keeps one state per request; a new

@@ -5,6 +5,7 @@
 
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "gdn_launch.h"
@@ -59,6 +60,41 @@ size_t prefill_workspace_bytes(int N) {
     if (N <= 0) return 0;
     return ((size_t)(N + 2) * sizeof(int32_t) + 255) / 256 * 256;
 }
+
+// Scratch of gdn_prefill_varlen_noalloc: the prefill workspace of up to
+// kScratchMaxSeqs sequences in a file-scope device array, one copy per GPU,
+// held until the process ends.  Host code uses it only through the device
+// address hipGetSymbolAddress returns (the array's name on the host is a
+// stand-in, not a device address).
+constexpr int kScratchMaxSeqs = 16384;
+constexpr size_t kScratchBytes = ((size_t)(kScratchMaxSeqs + 2) * sizeof(int32_t) + 255) / 256 * 256;
+static __device__ __align__(256) int32_t scratch[kScratchBytes / sizeof(int32_t)];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+// The current device's address of `scratch`, looked up once per device with
+// that device current.
+hipError_t scratch_address(void** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
+
+}  // namespace
 
 }  // namespace gdn
 
@@ -181,6 +217,29 @@ int gdn_prefill_varlen(const void* q, const void* k, const void* v, const float*
     gdn::PrefillArgs a{q, k, v, g, beta, cu_seqlens, initial_state, final_state, o,
                        N, T, H_qk, H_v, D_k, chunk, scale, workspace, nullptr, 0, false};
     hipError_t e = gdn::launch_prefill(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(GDN_EHIP, "prefill launch failed: %s", hipGetErrorString(e));
+    return GDN_OK;
+}
+
+int gdn_prefill_varlen_noalloc(const void* q, const void* k, const void* v, const float* g,
+                               const float* beta, const int32_t* cu_seqlens, const float* initial_state,
+                               float* final_state, void* o, int N, int T, int H_qk, int H_v, int D_k,
+                               int D_v, int chunk, float scale, void* stream) {
+    g_last_error.clear();
+    bool noop;
+    if (int st = check_prefill(q, k, v, g, beta, cu_seqlens, initial_state, final_state, o, N, T, H_qk, H_v,
+                               D_k, D_v, chunk, &noop))
+        return st;
+    if (noop) return GDN_OK;
+    if (N > gdn::kScratchMaxSeqs)
+        return fail(GDN_EWORKSPACE, "N = %d sequences exceeds the %d the no-allocation entry point's "
+                    "static scratch holds (use gdn_prefill_varlen with a workspace)", N, gdn::kScratchMaxSeqs);
+    void* ws = nullptr;
+    hipError_t e = gdn::scratch_address(&ws);
+    if (e != hipSuccess) return fail(GDN_EHIP, "scratch lookup failed: %s", hipGetErrorString(e));
+    gdn::PrefillArgs a{q, k, v, g, beta, cu_seqlens, initial_state, final_state, o,
+                       N, T, H_qk, H_v, D_k, chunk, scale, ws, nullptr, 0, false};
+    e = gdn::launch_prefill(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail(GDN_EHIP, "prefill launch failed: %s", hipGetErrorString(e));
     return GDN_OK;
 }

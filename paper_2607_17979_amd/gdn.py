@@ -25,13 +25,14 @@ __all__ = [
     "gdn_prefill_varlen",
     "gdn_prefill_varlen_indexed",
     "gdn_decode_multitoken",
+    "gdn_prefill_varlen_noalloc",
     "workspace_fault",
     "EXPORTED_SYMBOLS",
 ]
 
 EXPORTED_SYMBOLS = ("gdn_last_error", "gdn_abi_version", "gdn_decode", "gdn_decode_indexed",
                     "gdn_prefill_workspace_size", "gdn_prefill_varlen", "gdn_prefill_varlen_indexed",
-                    "gdn_decode_multitoken")
+                    "gdn_decode_multitoken", "gdn_prefill_varlen_noalloc")
 
 _STATUS = {0: "GDN_OK", -1: "GDN_EINVAL", -2: "GDN_EUNSUPPORTED", -3: "GDN_EALIGN",
            -4: "GDN_EWORKSPACE", -5: "GDN_EHIP"}
@@ -75,6 +76,9 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.gdn_prefill_varlen_indexed.restype = ci
     lib.gdn_prefill_varlen_indexed.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                                ci, ci, ci, ci, ci, ci, ci, ci, cf, vp, sz, vp]
+    lib.gdn_prefill_varlen_noalloc.restype = ci
+    lib.gdn_prefill_varlen_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                               ci, ci, ci, ci, ci, ci, ci, cf, vp]
     lib.gdn_decode_multitoken.restype = ci
     lib.gdn_decode_multitoken.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp,
                                           ci, ci, ci, ci, ci, ci, cf, vp, sz, vp]
@@ -327,3 +331,33 @@ def gdn_decode_multitoken(q, k, v, g, beta, cu_seqlens, state, o, scale: float =
                                      _stream(q, stream)))
     return workspace
 
+
+def gdn_prefill_varlen_noalloc(q, k, v, g, beta, cu_seqlens, initial_state, final_state, o,
+                               scale: float = 1.0, chunk: Optional[int] = None, stream=None) -> None:
+    """gdn_prefill_varlen without a workspace argument (see include/gdn.h): the
+    library's static per-GPU scratch serves instead, nothing is allocated, N
+    is at most 16,384; calls must not overlap in time on one GPU."""
+    import torch
+
+    T, H_qk, D = q.shape
+    H_v = v.shape[1]
+    N = cu_seqlens.shape[0] - 1
+    dev = q.device
+    if dev.type != "cuda":
+        raise ValueError("tensors must be on a GPU device")
+    _need(q, "q", torch.bfloat16, (T, H_qk, D), dev)
+    _need(k, "k", torch.bfloat16, (T, H_qk, D), dev)
+    _need(v, "v", torch.bfloat16, (T, H_v, D), dev)
+    _need(g, "g", torch.float32, (T, H_v), dev)
+    _need(beta, "beta", torch.float32, (T, H_v), dev)
+    _need(cu_seqlens, "cu_seqlens", torch.int32, (N + 1,), dev)
+    if initial_state is not None:
+        _need(initial_state, "initial_state", torch.float32, (N, H_v, D, D), dev)
+    _need(final_state, "final_state", torch.float32, (N, H_v, D, D), dev)
+    _need(o, "o", torch.bfloat16, (T, H_v, D), dev)
+    chunk = default_chunk(D) if chunk is None else chunk
+    lib = load_library()
+    _check(lib.gdn_prefill_varlen_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
+                                          _ptr(cu_seqlens), _ptr(initial_state), _ptr(final_state),
+                                          _ptr(o), N, T, H_qk, H_v, D, D, chunk, float(scale),
+                                          _stream(q, stream)))

@@ -59,6 +59,10 @@ int main() {
             st = gdn_decode_multitoken(P(0), P(1), P(2), (const float*)P(3), (const float*)P(4),
                                        (const int32_t*)P(5), (float*)P(6), P(7), I(8), I(9), I(10), I(11), I(12),
                                        I(13), F(14), P(15), Z(16), P(17));
+        } else if (fn == "gdn_prefill_varlen_noalloc") {
+            st = gdn_prefill_varlen_noalloc(P(0), P(1), P(2), (const float*)P(3), (const float*)P(4),
+                                            (const int32_t*)P(5), (const float*)P(6), (float*)P(7), P(8), I(9),
+                                            I(10), I(11), I(12), I(13), I(14), I(15), F(16), P(17));
         } else if (fn == "gdn_abi_version") {
             st = gdn_abi_version();
         } else {

@@ -228,3 +228,30 @@ def test_decode_multitoken_empty_is_noop(lib):
     assert multitoken(lib, q=None, k=None, v=None, g=None, beta=None, cu=None, state=None, o=None,
                       N=0, T=0, ws=None, ws_bytes=0) == OK
 
+
+def noalloc(lib, q=P, k=P, v=P, g=P, beta=P, cu=P, init=None, fin=P, o=P, N=3, T=10, H_qk=1, H_v=2,
+            Dk=128, Dv=128, chunk=64):
+    return lib.gdn_prefill_varlen_noalloc(q, k, v, g, beta, cu, init, fin, o, N, T, H_qk, H_v, Dk, Dv,
+                                          chunk, 1.0, None)
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(N=-1), EINVAL, "must be >= 0"),
+    (dict(H_qk=3, H_v=4), EINVAL, "multiple"),
+    (dict(chunk=32), EUNSUP, "chunk 32"),
+    (dict(cu=None), EINVAL, "cu_seqlens is NULL"),
+    (dict(fin=None), EINVAL, "final_state is NULL"),
+    (dict(init=P, fin=P + 1024), EINVAL, "overlap"),
+    (dict(q=None), EINVAL, "q is NULL"),
+    (dict(N=16385, T=16385), EWS, "16384"),
+])
+def test_prefill_noalloc_rejects(lib, kw, status, msg):
+    """The no-allocation entry point checks its arguments as gdn_prefill_varlen
+    does, and rejects more sequences than its static scratch holds, all on the
+    host before any HIP call."""
+    assert noalloc(lib, **kw) == status
+    assert msg in gdn.gdn_last_error()
+
+
+def test_prefill_noalloc_zero_sequences_is_noop(lib):
+    assert noalloc(lib, q=None, k=None, v=None, g=None, beta=None, cu=None, fin=None, o=None, N=0, T=0) == OK

@@ -94,6 +94,12 @@ def _cases():
         rec = _Recorder()
         helper(rec)  # defaults pass every check
         cases.append((_line(*rec.calls[0]), abi.OK, "", True))
+    # the no-allocation entry point: its checks only (its launch needs a GPU)
+    params = [m for m in abi.test_prefill_noalloc_rejects.pytestmark if m.name == "parametrize"][0].args[1]
+    for kw, status, msg in params:
+        rec = _Recorder()
+        abi.noalloc(rec, **kw)
+        cases.append((_line(*rec.calls[0]), status, msg, False))
     for kw in (dict(q=None, k=None, v=None, g=None, beta=None, state=None, o=None, B=0),):
         rec = _Recorder()
         abi.decode(rec, **kw)
