@@ -62,6 +62,21 @@ typedef enum gdn_status {
     GDN_EHIP = -5          /* a HIP runtime call or kernel launch failed */
 } gdn_status;
 
+/* Flags of the _ex entry points (bitwise or). */
+enum gdn_flags {
+    /* q and k are not assumed L2-normalised: each (token, q/k head) row x is
+     * replaced by bf16(x * r), r = 1 / sqrt(sum_i x_i^2 + 1e-6), computed in
+     * fp32 from the bf16 inputs (sum in index order, correctly rounded square
+     * root and division, then round to nearest even), before any other use. */
+    GDN_QK_L2NORM = 1,
+    /* g and beta hold logits a, b: g = -softplus(a) (so alpha = exp(g) =
+     * sigmoid(-a)) and beta = sigmoid(b), computed in fp32 in the kernel. */
+    GDN_GATE_LOGITS = 2,
+    /* prefill only: the caller promises every sequence has at most 8 tokens
+     * (a multi-token decode step, see gdn_decode_multitoken). */
+    GDN_SHORT_ONLY = 4
+};
+
 /* Message for the most recent non-OK status returned on the calling host
  * thread ("" if none).  The pointer stays valid until the next library call
  * on that thread. */
@@ -264,6 +279,59 @@ GDN_API int gdn_decode_multitoken(const void* q, const void* k, const void* v,
                        float* state, void* o,
                        int N, int T, int H_qk, int H_v, int D_k, int D_v,
                        float scale,
+                       void* workspace, size_t workspace_bytes,
+                       void* stream);
+
+/*
+ * gdn_decode_ex -- gdn_decode and gdn_decode_indexed with an input prologue
+ * fused into the kernel (paper: "Final Kernel Analysis", GDN prefill, where
+ * the gate and beta preprocessing is a helper kernel of its own; here it is
+ * part of the one launch).
+ *
+ *   state_idx  NULL: `state` is fp32 [B, H_v, D, D], one state per batch entry
+ *              (gdn_decode; P is ignored).  Otherwise `state` is a pool of P
+ *              slots and state_idx int32 [B] names each entry's slot
+ *              (gdn_decode_indexed, same rules).
+ *   flags      GDN_QK_L2NORM and/or GDN_GATE_LOGITS (see enum gdn_flags);
+ *              0 gives gdn_decode / gdn_decode_indexed bit for bit.
+ *
+ * Other arguments and errors as gdn_decode / gdn_decode_indexed, plus
+ * GDN_EINVAL for other flag bits.
+ */
+GDN_API int gdn_decode_ex(const void* q, const void* k, const void* v,
+               const float* g, const float* beta,
+               float* state, const int32_t* state_idx, int P, void* o,
+               int B, int H_qk, int H_v, int D_k, int D_v,
+               float scale, int flags, void* stream);
+
+/*
+ * gdn_prefill_varlen_ex -- gdn_prefill_varlen, gdn_prefill_varlen_indexed and
+ * gdn_decode_multitoken with the input prologue of gdn_decode_ex fused into
+ * the kernels.
+ *
+ *   state_idx  NULL: initial_state / final_state as gdn_prefill_varlen.
+ *              Otherwise final_state is a pool of P slots updated in place
+ *              (initial_state must be NULL or equal final_state) and
+ *              state_idx int32 [N] names each sequence's slot
+ *              (gdn_prefill_varlen_indexed, same rules).
+ *   flags      GDN_QK_L2NORM, GDN_GATE_LOGITS, GDN_SHORT_ONLY (the
+ *              gdn_decode_multitoken route: D = 128, T <= 8 N, the state
+ *              updated in place, so initial_state must be NULL or equal
+ *              final_state).  0 gives the plain entry points bit for bit.
+ *   workspace  gdn_prefill_workspace_size(N, T, H_v, D, D, chunk) bytes, as
+ *              gdn_prefill_varlen (same fault word).
+ *
+ * Other arguments and errors as the corresponding entry point, plus
+ * GDN_EINVAL for other flag bits.
+ */
+GDN_API int gdn_prefill_varlen_ex(const void* q, const void* k, const void* v,
+                       const float* g, const float* beta,
+                       const int32_t* cu_seqlens,
+                       const float* initial_state, float* final_state,
+                       const int32_t* state_idx, int P,
+                       void* o,
+                       int N, int T, int H_qk, int H_v, int D_k, int D_v,
+                       int chunk, float scale, int flags,
                        void* workspace, size_t workspace_bytes,
                        void* stream);
 

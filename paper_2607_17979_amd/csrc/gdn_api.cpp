@@ -8,7 +8,12 @@
 #include <mutex>
 #include <string>
 
+#include "gdn_device.h"
 #include "gdn_launch.h"
+
+static_assert(GDN_QK_L2NORM == gdn::kFlagQkL2Norm && GDN_GATE_LOGITS == gdn::kFlagGateLogits &&
+                  GDN_SHORT_ONLY == gdn::kFlagShortOnly,
+              "the ABI's flag bits are the kernels'");
 
 namespace {
 
@@ -102,12 +107,11 @@ extern "C" {
 
 const char* gdn_last_error(void) { return g_last_error.c_str(); }
 
-int gdn_abi_version(void) { return 200; }
+int gdn_abi_version(void) { return 210; }
 
-int gdn_decode(const void* q, const void* k, const void* v, const float* g, const float* beta,
-               float* state, void* o, int B, int H_qk, int H_v, int D_k, int D_v, float scale,
-               void* stream) {
-    g_last_error.clear();
+static int decode_impl(const void* q, const void* k, const void* v, const float* g, const float* beta,
+                       float* state, void* o, int B, int H_qk, int H_v, int D_k, int D_v, float scale,
+                       int flags, void* stream) {
     if (B < 0) return fail(GDN_EINVAL, "B must be >= 0 (got %d)", B);
     if (int st = check_heads(H_qk, H_v, D_k, D_v)) return st;
     if (B == 0) return GDN_OK;
@@ -118,16 +122,15 @@ int gdn_decode(const void* q, const void* k, const void* v, const float* g, cons
         (st = check_ptr16(state, "state")) || (st = check_ptr16(o, "o")) ||
         (st = check_ptr4(g, "g")) || (st = check_ptr4(beta, "beta")))
         return st;
-    gdn::DecodeArgs a{q, k, v, g, beta, state, o, B, H_qk, H_v, D_k, scale, nullptr, 0};
+    gdn::DecodeArgs a{q, k, v, g, beta, state, o, B, H_qk, H_v, D_k, scale, nullptr, 0, flags};
     hipError_t e = gdn::launch_decode(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail(GDN_EHIP, "decode launch failed: %s", hipGetErrorString(e));
     return GDN_OK;
 }
 
-int gdn_decode_indexed(const void* q, const void* k, const void* v, const float* g, const float* beta,
-                       float* state_pool, const int32_t* state_idx, void* o, int B, int P, int H_qk,
-                       int H_v, int D_k, int D_v, float scale, void* stream) {
-    g_last_error.clear();
+static int decode_indexed_impl(const void* q, const void* k, const void* v, const float* g,
+                               const float* beta, float* state_pool, const int32_t* state_idx, void* o, int B,
+                               int P, int H_qk, int H_v, int D_k, int D_v, float scale, int flags, void* stream) {
     if (B < 0) return fail(GDN_EINVAL, "B must be >= 0 (got %d)", B);
     if (P < 0) return fail(GDN_EINVAL, "P must be >= 0 (got %d)", P);
     if (int st = check_heads(H_qk, H_v, D_k, D_v)) return st;
@@ -141,7 +144,7 @@ int gdn_decode_indexed(const void* q, const void* k, const void* v, const float*
         (st = check_ptr16(state_pool, "state_pool")) || (st = check_ptr4(state_idx, "state_idx")) ||
         (st = check_ptr16(o, "o")) || (st = check_ptr4(g, "g")) || (st = check_ptr4(beta, "beta")))
         return st;
-    gdn::DecodeArgs a{q, k, v, g, beta, state_pool, o, B, H_qk, H_v, D_k, scale, state_idx, P};
+    gdn::DecodeArgs a{q, k, v, g, beta, state_pool, o, B, H_qk, H_v, D_k, scale, state_idx, P, flags};
     hipError_t e = gdn::launch_decode(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail(GDN_EHIP, "decode launch failed: %s", hipGetErrorString(e));
     return GDN_OK;
@@ -198,12 +201,10 @@ int check_prefill(const void* q, const void* k, const void* v, const float* g, c
 
 extern "C" {
 
-int gdn_prefill_varlen(const void* q, const void* k, const void* v, const float* g,
-                       const float* beta, const int32_t* cu_seqlens, const float* initial_state,
-                       float* final_state, void* o, int N, int T, int H_qk, int H_v, int D_k,
-                       int D_v, int chunk, float scale, void* workspace, size_t workspace_bytes,
-                       void* stream) {
-    g_last_error.clear();
+static int prefill_impl(const void* q, const void* k, const void* v, const float* g, const float* beta,
+                        const int32_t* cu_seqlens, const float* initial_state, float* final_state, void* o,
+                        int N, int T, int H_qk, int H_v, int D_k, int D_v, int chunk, float scale, int flags,
+                        void* workspace, size_t workspace_bytes, void* stream) {
     bool noop;
     if (int st = check_prefill(q, k, v, g, beta, cu_seqlens, initial_state, final_state, o, N, T, H_qk, H_v,
                                D_k, D_v, chunk, &noop))
@@ -215,7 +216,7 @@ int gdn_prefill_varlen(const void* q, const void* k, const void* v, const float*
                     workspace_bytes, workspace == nullptr ? " (NULL)" : "");
     if (!aligned(workspace, 256)) return fail(GDN_EALIGN, "workspace is not 256-byte aligned");
     gdn::PrefillArgs a{q, k, v, g, beta, cu_seqlens, initial_state, final_state, o,
-                       N, T, H_qk, H_v, D_k, chunk, scale, workspace, nullptr, 0, false};
+                       N, T, H_qk, H_v, D_k, chunk, scale, workspace, nullptr, 0, false, flags};
     hipError_t e = gdn::launch_prefill(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail(GDN_EHIP, "prefill launch failed: %s", hipGetErrorString(e));
     return GDN_OK;
@@ -238,18 +239,17 @@ int gdn_prefill_varlen_noalloc(const void* q, const void* k, const void* v, cons
     hipError_t e = gdn::scratch_address(&ws);
     if (e != hipSuccess) return fail(GDN_EHIP, "scratch lookup failed: %s", hipGetErrorString(e));
     gdn::PrefillArgs a{q, k, v, g, beta, cu_seqlens, initial_state, final_state, o,
-                       N, T, H_qk, H_v, D_k, chunk, scale, ws, nullptr, 0, false};
+                       N, T, H_qk, H_v, D_k, chunk, scale, ws, nullptr, 0, false, 0};
     e = gdn::launch_prefill(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail(GDN_EHIP, "prefill launch failed: %s", hipGetErrorString(e));
     return GDN_OK;
 }
 
-int gdn_prefill_varlen_indexed(const void* q, const void* k, const void* v, const float* g,
-                               const float* beta, const int32_t* cu_seqlens, float* state_pool,
-                               const int32_t* state_idx, void* o, int N, int T, int P, int H_qk,
-                               int H_v, int D_k, int D_v, int chunk, float scale, void* workspace,
-                               size_t workspace_bytes, void* stream) {
-    g_last_error.clear();
+static int prefill_indexed_impl(const void* q, const void* k, const void* v, const float* g,
+                                const float* beta, const int32_t* cu_seqlens, float* state_pool,
+                                const int32_t* state_idx, void* o, int N, int T, int P, int H_qk, int H_v,
+                                int D_k, int D_v, int chunk, float scale, int flags, void* workspace,
+                                size_t workspace_bytes, void* stream) {
     if (N < 0 || T < 0) return fail(GDN_EINVAL, "N and T must be >= 0 (N=%d, T=%d)", N, T);
     if (P < 0) return fail(GDN_EINVAL, "P must be >= 0 (got %d)", P);
     if (int st = check_heads(H_qk, H_v, D_k, D_v)) return st;
@@ -276,17 +276,16 @@ int gdn_prefill_varlen_indexed(const void* q, const void* k, const void* v, cons
                     workspace_bytes, workspace == nullptr ? " (NULL)" : "");
     if (!aligned(workspace, 256)) return fail(GDN_EALIGN, "workspace is not 256-byte aligned");
     gdn::PrefillArgs a{q, k, v, g, beta, cu_seqlens, state_pool, state_pool, o,
-                       N, T, H_qk, H_v, D_k, chunk, scale, workspace, state_idx, P, false};
+                       N, T, H_qk, H_v, D_k, chunk, scale, workspace, state_idx, P, false, flags};
     hipError_t e = gdn::launch_prefill(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail(GDN_EHIP, "prefill launch failed: %s", hipGetErrorString(e));
     return GDN_OK;
 }
 
-int gdn_decode_multitoken(const void* q, const void* k, const void* v, const float* g,
-                          const float* beta, const int32_t* cu_seqlens, float* state, void* o, int N,
-                          int T, int H_qk, int H_v, int D_k, int D_v, float scale, void* workspace,
-                          size_t workspace_bytes, void* stream) {
-    g_last_error.clear();
+static int multitoken_impl(const void* q, const void* k, const void* v, const float* g, const float* beta,
+                           const int32_t* cu_seqlens, float* state, const int32_t* state_idx, int P, void* o,
+                           int N, int T, int H_qk, int H_v, int D_k, int D_v, float scale, int flags,
+                           void* workspace, size_t workspace_bytes, void* stream) {
     if (N < 0 || T < 0) return fail(GDN_EINVAL, "N and T must be >= 0 (N=%d, T=%d)", N, T);
     if (int st = check_heads(H_qk, H_v, D_k, D_v)) return st;
     if (D_k != 128) return fail(GDN_EUNSUPPORTED, "multi-token decode runs for head dim 128 (got %d)", D_k);
@@ -298,6 +297,12 @@ int gdn_decode_multitoken(const void* q, const void* k, const void* v, const flo
         return fail(GDN_EINVAL, "problem too large (N=%d, H_v=%d)", N, H_v);
     int st;
     if ((st = check_ptr4(cu_seqlens, "cu_seqlens")) || (st = check_ptr16(state, "state"))) return st;
+    if (state_idx != nullptr) {
+        if (P < 0) return fail(GDN_EINVAL, "P must be >= 0 (got %d)", P);
+        if (P == 0) return GDN_OK;
+        if ((long long)P * H_v > (1LL << 30)) return fail(GDN_EINVAL, "P * H_v = %lld too large", (long long)P * H_v);
+        if ((st = check_ptr4(state_idx, "state_idx"))) return st;
+    }
     if (T > 0) {
         if ((st = check_ptr16(q, "q")) || (st = check_ptr16(k, "k")) || (st = check_ptr16(v, "v")) ||
             (st = check_ptr16(o, "o")) || (st = check_ptr4(g, "g")) || (st = check_ptr4(beta, "beta")))
@@ -309,10 +314,92 @@ int gdn_decode_multitoken(const void* q, const void* k, const void* v, const flo
                     workspace_bytes, workspace == nullptr ? " (NULL)" : "");
     if (!aligned(workspace, 256)) return fail(GDN_EALIGN, "workspace is not 256-byte aligned");
     gdn::PrefillArgs a{q, k, v, g, beta, cu_seqlens, state, state, o,
-                       N, T, H_qk, H_v, D_k, chunk_for(D_k), scale, workspace, nullptr, 0, true};
+                       N, T, H_qk, H_v, D_k, chunk_for(D_k), scale, workspace, state_idx, P, true, flags};
     hipError_t e = gdn::launch_prefill(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail(GDN_EHIP, "multi-token decode launch failed: %s", hipGetErrorString(e));
     return GDN_OK;
+}
+
+int gdn_decode(const void* q, const void* k, const void* v, const float* g, const float* beta,
+               float* state, void* o, int B, int H_qk, int H_v, int D_k, int D_v, float scale,
+               void* stream) {
+    g_last_error.clear();
+    return decode_impl(q, k, v, g, beta, state, o, B, H_qk, H_v, D_k, D_v, scale, 0, stream);
+}
+
+int gdn_decode_indexed(const void* q, const void* k, const void* v, const float* g, const float* beta,
+                       float* state_pool, const int32_t* state_idx, void* o, int B, int P, int H_qk,
+                       int H_v, int D_k, int D_v, float scale, void* stream) {
+    g_last_error.clear();
+    return decode_indexed_impl(q, k, v, g, beta, state_pool, state_idx, o, B, P, H_qk, H_v, D_k, D_v, scale, 0,
+                               stream);
+}
+
+int gdn_prefill_varlen(const void* q, const void* k, const void* v, const float* g,
+                       const float* beta, const int32_t* cu_seqlens, const float* initial_state,
+                       float* final_state, void* o, int N, int T, int H_qk, int H_v, int D_k,
+                       int D_v, int chunk, float scale, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+    g_last_error.clear();
+    return prefill_impl(q, k, v, g, beta, cu_seqlens, initial_state, final_state, o, N, T, H_qk, H_v, D_k, D_v,
+                        chunk, scale, 0, workspace, workspace_bytes, stream);
+}
+
+int gdn_prefill_varlen_indexed(const void* q, const void* k, const void* v, const float* g,
+                               const float* beta, const int32_t* cu_seqlens, float* state_pool,
+                               const int32_t* state_idx, void* o, int N, int T, int P, int H_qk,
+                               int H_v, int D_k, int D_v, int chunk, float scale, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+    g_last_error.clear();
+    return prefill_indexed_impl(q, k, v, g, beta, cu_seqlens, state_pool, state_idx, o, N, T, P, H_qk, H_v, D_k,
+                                D_v, chunk, scale, 0, workspace, workspace_bytes, stream);
+}
+
+int gdn_decode_multitoken(const void* q, const void* k, const void* v, const float* g,
+                          const float* beta, const int32_t* cu_seqlens, float* state, void* o, int N,
+                          int T, int H_qk, int H_v, int D_k, int D_v, float scale, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+    g_last_error.clear();
+    return multitoken_impl(q, k, v, g, beta, cu_seqlens, state, nullptr, 0, o, N, T, H_qk, H_v, D_k, D_v, scale,
+                           0, workspace, workspace_bytes, stream);
+}
+
+int gdn_decode_ex(const void* q, const void* k, const void* v, const float* g, const float* beta,
+                  float* state, const int32_t* state_idx, int P, void* o, int B, int H_qk, int H_v, int D_k,
+                  int D_v, float scale, int flags, void* stream) {
+    g_last_error.clear();
+    if (flags & ~(GDN_QK_L2NORM | GDN_GATE_LOGITS))
+        return fail(GDN_EINVAL, "unknown or unsupported flags 0x%x for gdn_decode_ex", flags);
+    if (state_idx == nullptr)
+        return decode_impl(q, k, v, g, beta, state, o, B, H_qk, H_v, D_k, D_v, scale, flags, stream);
+    return decode_indexed_impl(q, k, v, g, beta, state, state_idx, o, B, P, H_qk, H_v, D_k, D_v, scale, flags,
+                               stream);
+}
+
+int gdn_prefill_varlen_ex(const void* q, const void* k, const void* v, const float* g, const float* beta,
+                          const int32_t* cu_seqlens, const float* initial_state, float* final_state,
+                          const int32_t* state_idx, int P, void* o, int N, int T, int H_qk, int H_v, int D_k,
+                          int D_v, int chunk, float scale, int flags, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+    g_last_error.clear();
+    if (flags & ~(GDN_QK_L2NORM | GDN_GATE_LOGITS | GDN_SHORT_ONLY))
+        return fail(GDN_EINVAL, "unknown flags 0x%x for gdn_prefill_varlen_ex", flags);
+    const int prologue = flags & (GDN_QK_L2NORM | GDN_GATE_LOGITS);
+    if ((state_idx != nullptr || (flags & GDN_SHORT_ONLY)) && initial_state != nullptr &&
+        initial_state != final_state)
+        return fail(GDN_EINVAL, "with state_idx or GDN_SHORT_ONLY the state is updated in place: "
+                    "initial_state must be NULL or equal final_state");
+    if (flags & GDN_SHORT_ONLY) {
+        if (D_k == 128 && D_v == 128 && chunk != 64)
+            return fail(GDN_EUNSUPPORTED, "chunk %d unsupported for head dim 128 (use 64)", chunk);
+        return multitoken_impl(q, k, v, g, beta, cu_seqlens, final_state, state_idx, P, o, N, T, H_qk, H_v, D_k,
+                               D_v, scale, prologue, workspace, workspace_bytes, stream);
+    }
+    if (state_idx != nullptr)
+        return prefill_indexed_impl(q, k, v, g, beta, cu_seqlens, final_state, state_idx, o, N, T, P, H_qk, H_v,
+                                    D_k, D_v, chunk, scale, prologue, workspace, workspace_bytes, stream);
+    return prefill_impl(q, k, v, g, beta, cu_seqlens, initial_state, final_state, o, N, T, H_qk, H_v, D_k, D_v,
+                        chunk, scale, prologue, workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

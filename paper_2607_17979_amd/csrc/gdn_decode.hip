@@ -34,7 +34,7 @@ __global__ __launch_bounds__(256) void decode_kernel(
     const uint16_t* __restrict__ v, const float* __restrict__ g,
     const float* __restrict__ beta, float* __restrict__ state,
     uint16_t* __restrict__ o, int H_qk, int H_v, int blocks_per_head, float scale,
-    const int32_t* __restrict__ idx, int P) {
+    const int32_t* __restrict__ idx, int P, int flags) {
     constexpr int F4_ROW = D / 4;
     constexpr int LPR = F4_ROW < 8 ? F4_ROW : 8;
     constexpr int J = F4_ROW / LPR;
@@ -59,16 +59,24 @@ __global__ __launch_bounds__(256) void decode_kernel(
     const int sub = lane / LPR;
     const int c = lane % LPR;
 
-    // q and k slices for this lane's columns, widened to fp32.
+    // q and k slices for this lane's columns, widened to fp32 (L2-normalised
+    // and rounded to bf16 again first, with the prologue flag).
     const uint16_t* kp = k + ((size_t)b * H_qk + hq) * D;
     const uint16_t* qp = q + ((size_t)b * H_qk + hq) * D;
+    const bool norm = (flags & kFlagQkL2Norm) != 0;
+    const float rk = norm ? row_inv_norm<D>(kp) : 1.f;
+    const float rq = norm ? row_inv_norm<D>(qp) : 1.f;
     float kf[J][4], qf[J][4];
     float kq = 0.f;
 #pragma unroll
     for (int j = 0; j < J; ++j) {
         const int col = (j * LPR + c) * 4;
-        const uint2 kk = *reinterpret_cast<const uint2*>(kp + col);
-        const uint2 qq = *reinterpret_cast<const uint2*>(qp + col);
+        uint2 kk = *reinterpret_cast<const uint2*>(kp + col);
+        uint2 qq = *reinterpret_cast<const uint2*>(qp + col);
+        if (norm) {
+            kk = uint2{scale_bf16x2(kk.x, rk), scale_bf16x2(kk.y, rk)};
+            qq = uint2{scale_bf16x2(qq.x, rq), scale_bf16x2(qq.y, rq)};
+        }
         kf[j][0] = bf16_to_f32(kk.x & 0xFFFF); kf[j][1] = bf16_to_f32(kk.x >> 16);
         kf[j][2] = bf16_to_f32(kk.y & 0xFFFF); kf[j][3] = bf16_to_f32(kk.y >> 16);
         qf[j][0] = bf16_to_f32(qq.x & 0xFFFF); qf[j][1] = bf16_to_f32(qq.x >> 16);
@@ -78,8 +86,9 @@ __global__ __launch_bounds__(256) void decode_kernel(
     }
     kq = group_sum<LPR>(kq);
 
-    const float alpha = fast_exp(g[head]);
-    const float bt = beta[head];
+    const bool logits = (flags & kFlagGateLogits) != 0;
+    const float alpha = fast_exp(logits ? gate_from_logit(g[head]) : g[head]);
+    const float bt = logits ? beta_from_logit(beta[head]) : beta[head];
     float* sp = state + (size_t)shead * D * D;
     const uint16_t* vp = v + (size_t)head * D;
     uint16_t* op = o + (size_t)head * D;
@@ -142,11 +151,11 @@ static hipError_t launch_decode_d(const DecodeArgs& a, hipStream_t stream) {
     if (a.state_idx != nullptr)
         hipLaunchKernelGGL((decode_kernel<D, 1, true>), grid, block, 0, stream, (const uint16_t*)a.q,
                            (const uint16_t*)a.k, (const uint16_t*)a.v, a.g, a.beta, a.state,
-                           (uint16_t*)a.o, a.H_qk, a.H_v, blocks_per_head, a.scale, a.state_idx, a.P);
+                           (uint16_t*)a.o, a.H_qk, a.H_v, blocks_per_head, a.scale, a.state_idx, a.P, a.flags);
     else
         hipLaunchKernelGGL((decode_kernel<D, 1, false>), grid, block, 0, stream, (const uint16_t*)a.q,
                            (const uint16_t*)a.k, (const uint16_t*)a.v, a.g, a.beta, a.state,
-                           (uint16_t*)a.o, a.H_qk, a.H_v, blocks_per_head, a.scale, nullptr, 0);
+                           (uint16_t*)a.o, a.H_qk, a.H_v, blocks_per_head, a.scale, nullptr, 0, a.flags);
     return hipGetLastError();
 }
 

@@ -25,6 +25,52 @@ __device__ __forceinline__ float fast_exp(float x) {
     return __builtin_amdgcn_exp2f(x * 1.4426950408889634f);
 }
 
+// ---- optional input prologue (the flags of the _ex entry points) ------------
+enum : int {
+    kFlagQkL2Norm = 1,      // q and k rows are L2-normalised in the kernel
+    kFlagGateLogits = 2,    // g and beta hold logits: g = -softplus(a), beta = sigmoid(b)
+    kFlagShortOnly = 4,     // prefill: every sequence has at most 8 tokens (multi-token decode)
+};
+
+// 1 / sqrt(sum of squares + 1e-6) of a row of D bf16 values in global memory,
+// summed in index order with one rounding per term (the square of a bf16
+// value is exact in fp32) and correctly rounded square root and division, so
+// that every kernel, and a host computation in the same order, gets the same
+// bits for the same row.
+template <int D>
+__device__ __forceinline__ float row_inv_norm(const uint16_t* row) {
+    float acc = 0.f;
+#pragma unroll
+    for (int s = 0; s < D / 8; ++s) {
+        const uint4 u = *reinterpret_cast<const uint4*>(row + 8 * s);
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float lo = __uint_as_float(w[e] << 16), hi = __uint_as_float(w[e] & 0xFFFF0000u);
+            acc = fmaf(lo, lo, acc);
+            acc = fmaf(hi, hi, acc);
+        }
+    }
+    return 1.0f / sqrtf(acc + 1e-6f);
+}
+
+// Two packed bf16 values times r, rounded to bf16 again (nearest even).
+__device__ __forceinline__ uint32_t scale_bf16x2(uint32_t w, float r) {
+    const uint32_t lo = f32_to_bf16(__uint_as_float(w << 16) * r);
+    const uint32_t hi = f32_to_bf16(__uint_as_float(w & 0xFFFF0000u) * r);
+    return lo | (hi << 16);
+}
+__device__ __forceinline__ uint4 scale_bf16x8(const uint4& u, float r) {
+    return uint4{scale_bf16x2(u.x, r), scale_bf16x2(u.y, r), scale_bf16x2(u.z, r), scale_bf16x2(u.w, r)};
+}
+
+// g = log alpha = -softplus(a) for a gate logit a, in fp32.
+__device__ __forceinline__ float gate_from_logit(float a) {
+    return -(fmaxf(a, 0.f) + log1pf(expf(-fabsf(a))));
+}
+// beta = sigmoid(b) for a logit b, in fp32.
+__device__ __forceinline__ float beta_from_logit(float b) { return 1.f / (1.f + expf(-b)); }
+
 // DPP lane moves inside a row of 16 lanes.
 template <int CTRL>
 __device__ __forceinline__ float dpp(float x) {

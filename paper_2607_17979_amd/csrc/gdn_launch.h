@@ -20,6 +20,7 @@ struct DecodeArgs {
     float scale;
     const int32_t* state_idx;  // NULL: state b is batch entry b; else a pool slot per entry
     int P;                     // pool slots (with state_idx)
+    int flags;                 // input prologue: kFlagQkL2Norm | kFlagGateLogits (gdn_device.h)
 };
 
 struct PrefillArgs {
@@ -40,6 +41,7 @@ struct PrefillArgs {
     bool short_only;           // the caller's promise that no sequence exceeds kRecurMax:
                                // only the token-by-token launch runs, and a longer sequence
                                // is skipped and flagged (wait-fault word bit 1)
+    int flags;                 // input prologue: kFlagQkL2Norm | kFlagGateLogits (gdn_device.h)
 };
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);

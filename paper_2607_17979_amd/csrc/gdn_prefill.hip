@@ -99,7 +99,7 @@ __global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
     const float* __restrict__ beta, const int32_t* __restrict__ cu,
     const int32_t* __restrict__ order, const float* initial_state, float* final_state,
     uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale,
-    const int32_t* __restrict__ state_idx, int P_slots) {
+    const int32_t* __restrict__ state_idx, int P_slots, int flags) {
     typedef Cfg<D, C> P;
     constexpr int KD = P::KD, KC = P::KC;
     typedef typename Frag<KD>::type FD;
@@ -170,9 +170,14 @@ __global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
             const int r = i / P::SEGS, seg = i - r * P::SEGS;
             pq[it] = pk[it] = pv[it] = uint4{0, 0, 0, 0};
             if (i < C * P::SEGS && r < Lc) {
-                const size_t tq = (size_t)(tb + r) * qk_stride + (size_t)hq * D + seg * 8;
+                const size_t row = (size_t)(tb + r) * qk_stride + (size_t)hq * D;
+                const size_t tq = row + seg * 8;
                 pq[it] = *reinterpret_cast<const uint4*>(q + tq);
                 pk[it] = *reinterpret_cast<const uint4*>(k + tq);
+                if (flags & kFlagQkL2Norm) {
+                    pq[it] = scale_bf16x8(pq[it], row_inv_norm<D>(q + row));
+                    pk[it] = scale_bf16x8(pk[it], row_inv_norm<D>(k + row));
+                }
                 pv[it] = *reinterpret_cast<const uint4*>(v + (size_t)(tb + r) * v_stride + (size_t)h * D + seg * 8);
             }
         }
@@ -180,6 +185,10 @@ __global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
             const bool in = tid < Lc;
             pg = in ? g[(size_t)(tb + tid) * H_v + h] : 0.f;
             pb = in ? beta[(size_t)(tb + tid) * H_v + h] : 0.f;
+            if (in && (flags & kFlagGateLogits)) {
+                pg = gate_from_logit(pg);
+                pb = beta_from_logit(pb);
+            }
         }
     };
     if (seq_len > 0) load_chunk(0);
@@ -496,7 +505,7 @@ hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {
     hipLaunchKernelGGL((prefill_kernel<16, 16>), dim3((unsigned)(a.N * a.H_v)), dim3(P16::NT), 0,
                        stream, (const uint16_t*)a.q, (const uint16_t*)a.k, (const uint16_t*)a.v, a.g,
                        a.beta, a.cu_seqlens, (const int32_t*)order, a.initial_state, a.final_state,
-                       (uint16_t*)a.o, a.N, a.H_qk, a.H_v, a.scale, a.state_idx, a.P);
+                       (uint16_t*)a.o, a.N, a.H_qk, a.H_v, a.scale, a.state_idx, a.P, a.flags);
     return hipGetLastError();
 }
 

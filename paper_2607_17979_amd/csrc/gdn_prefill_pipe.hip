@@ -105,6 +105,7 @@ struct Smem {
     uint4 hs[NO][D / 32][NVT][64];    // per state wave: S0 hi operands of the chunk
     uint4 hu[NO][C / 32][NVT][64];    // per state wave: U hi operands of the chunk
     unsigned cnt[NCNT];
+    alignas(16) float rn[NP][2][C];   // per producer, with the q/k L2 norm: 1 / |row| of its K, Q rows
 };
 
 // Inclusive prefix sum over the 64 lanes of a wave (DPP row shifts, then row
@@ -295,8 +296,10 @@ __device__ __forceinline__ uint4 ld16(const void* base, unsigned byte_off) {
 // are recomputed per chunk instead of being kept live across the producer loop.
 // NSIG: waves that count each chunk done and each Q/V release (state plus
 // output waves); VB: value columns staged.
-template <int NSIG, int VB, class SM>
+// PRO: the input prologue (kFlagQkL2Norm, kFlagGateLogits).
+template <int NSIG, int VB, int PRO, class SM>
 __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, int lc, int m, int gq) {
+    constexpr bool NORM = (PRO & kFlagQkL2Norm) != 0;
     const int lane = m + 16 * gq;
     Slot& sl = sm.slot[pc.pw];
     float* scr = sm.scr[pc.pw];
@@ -316,17 +319,36 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
     const uint16_t* qc0 = pc.q + (size_t)tb * pc.qk_stride + (size_t)pc.hq * D;
     const unsigned qks = (unsigned)pc.qk_stride;
     const bool in = lane < L;
-    const float gl = in ? pc.g[(size_t)(tb + lane) * pc.H_v + pc.h] : 0.f;
-    const float bl = in ? pc.beta[(size_t)(tb + lane) * pc.H_v + pc.h] : 0.f;
-    auto load_frags = [&](const uint16_t* base, int b, uint4 (&f)[4]) {
+    float gl = in ? pc.g[(size_t)(tb + lane) * pc.H_v + pc.h] : 0.f;
+    float bl = in ? pc.beta[(size_t)(tb + lane) * pc.H_v + pc.h] : 0.f;
+    if ((PRO & kFlagGateLogits) && in) {
+        gl = gate_from_logit(gl);
+        bl = beta_from_logit(bl);
+    }
+    // With the q/k L2 norm: 1 / |row| of K and Q row `lane` (rows past the end
+    // repeat row L - 1, as the loads below do), for the fragments and the
+    // staged rows alike, so that both use the same bf16 values.
+    float* rnk = sm.rn[pc.pw][0];
+    float* rnq = sm.rn[pc.pw][1];
+    if constexpr (NORM) {
+        const unsigned roff = (unsigned)min(lane, L - 1) * qks;
+        rnk[lane] = row_inv_norm<D>(kc0 + roff);
+        rnq[lane] = row_inv_norm<D>(qc0 + roff);
+    }
+    auto load_frags = [&](const uint16_t* base, const float* rn, int b, uint4 (&f)[4]) {
         const unsigned off = (unsigned)min(16 * b + m, L - 1) * qks + 8u * gq;
 #pragma unroll
         for (int kq = 0; kq < 4; ++kq) f[kq] = ld16(base, 2u * off + 64u * kq);
+        if constexpr (NORM) {
+            const float r = rn[16 * b + m];
+#pragma unroll
+            for (int kq = 0; kq < 4; ++kq) f[kq] = scale_bf16x8(f[kq], r);
+        }
     };
     uint4 fk[NCT][4], fq[2][4];
 #pragma unroll
-    for (int b = 0; b < NCT; ++b) load_frags(kc0, b, fk[b]);
-    load_frags(qc0, 0, fq[0]);
+    for (int b = 0; b < NCT; ++b) load_frags(kc0, rnk, b, fk[b]);
+    load_frags(qc0, rnq, 0, fq[0]);
     const float gx = wave_prefix_sum(gl);
     const float glast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gx), C - 1));
     gam[lane] = gx;
@@ -342,7 +364,7 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
     uint2 pk[NBLK];
 #pragma unroll
     for (int b = 0; b < NCT; ++b) {
-        if (b + 1 < NCT) load_frags(qc0, b + 1, fq[(b + 1) & 1]);
+        if (b + 1 < NCT) load_frags(qc0, rnq, b + 1, fq[(b + 1) & 1]);
 #pragma unroll
         for (int jt = 0; jt <= b; ++jt) {
             f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
@@ -473,6 +495,11 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
         sk[it] = sq[it] = uint4{0, 0, 0, 0};
         sk[it] = ld16(kc0, 2u * off);
         sq[it] = ld16(qc0, 2u * off);
+        if constexpr (NORM) {
+            const int row = min(4 * it + gq, L - 1);
+            sk[it] = scale_bf16x8(sk[it], rnk[row]);
+            sq[it] = scale_bf16x8(sq[it], rnq[row]);
+        }
     }
     // K buffer x & 1 was last read by the update of chunk x - 2
     wait_ge(&sm.cnt[CNT_DONE], (unsigned)(x >= 2 ? NSIG * (x - 1) : 0), pc.fault);
@@ -507,13 +534,14 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
 // covers NS * NVT * 16 of the D value columns of its head, so a head is split
 // over VSPLIT = D / (16 NS NVT) workgroups (each repeating the producer work of
 // the head), which spreads few long sequences over more compute units.
-template <int NS, int NVT, int NO>
+template <int NS, int NVT, int NO, int PRO>
 __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const float* __restrict__ g, const float* __restrict__ beta, const int32_t* __restrict__ cu,
     const int32_t* __restrict__ order, const float* initial_state, float* final_state,
     uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale,
     const int32_t* __restrict__ state_idx, int P, int* fault) {
+    constexpr bool NORM = (PRO & kFlagQkL2Norm) != 0;
     constexpr int VW = 16 * NVT;        // value columns per state wave
     constexpr int VB = NS * VW;         // value columns per workgroup
     constexpr int VSPLIT = D / VB;
@@ -562,9 +590,14 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
             const int r = i / SEGS, seg = i - r * SEGS;
             uint4 rk = {0, 0, 0, 0}, rq = {0, 0, 0, 0};
             if (r < L0) {
-                const size_t tq = (size_t)(first.seq_beg + r) * qk_stride + (size_t)first.hq * D + seg * 8;
+                const size_t row = (size_t)(first.seq_beg + r) * qk_stride + (size_t)first.hq * D;
+                const size_t tq = row + seg * 8;
                 rk = *reinterpret_cast<const uint4*>(k + tq);
                 rq = *reinterpret_cast<const uint4*>(q + tq);
+                if constexpr (NORM) {
+                    rk = scale_bf16x8(rk, row_inv_norm<D>(k + row));
+                    rq = scale_bf16x8(rq, row_inv_norm<D>(q + row));
+                }
             }
             *reinterpret_cast<uint4*>(&sm.kb[0][r][swz(r, seg * 8)]) = rk;
             *reinterpret_cast<uint4*>(&sm.qb[r][swz(r, seg * 8)]) = rq;
@@ -986,7 +1019,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
             pc.vcb0 = it.vblock * VB;
             int mo = m, go = gq;
             asm volatile("" : "+v"(mo), "+v"(go));
-            produce_chunk<NS + NO, VB>(sm, pc, x, x - xbeg, mo, go);
+            produce_chunk<NS + NO, VB, PRO>(sm, pc, x, x - xbeg, mo, go);
         }
     }
 }
@@ -1006,16 +1039,28 @@ int device_compute_units() {
 
 // One workgroup per compute unit (the LDS use admits one), each walking its
 // work items; fewer items than compute units give one item per workgroup.
-template <int NS, int NVT, int NO>
-static hipError_t launch_pipe(const PrefillArgs& a, int32_t* order, hipStream_t stream) {
+template <int NS, int NVT, int NO, int PRO>
+static hipError_t launch_pipe_pro(const PrefillArgs& a, int32_t* order, hipStream_t stream) {
     constexpr int VSPLIT = pipe::D / (16 * NS * NVT);
     const long items = (long)a.N * a.H_v * VSPLIT;
     const long grid = std::min<long>(items, device_compute_units());
-    hipLaunchKernelGGL((pipe::prefill_pipe_kernel<NS, NVT, NO>), dim3((unsigned)grid),
+    hipLaunchKernelGGL((pipe::prefill_pipe_kernel<NS, NVT, NO, PRO>), dim3((unsigned)grid),
                        dim3(64 * (NS + NO + pipe::NP)), 0, stream, (const uint16_t*)a.q, (const uint16_t*)a.k,
                        (const uint16_t*)a.v, a.g, a.beta, a.cu_seqlens, order, a.initial_state, a.final_state,
                        (uint16_t*)a.o, a.N, a.H_qk, a.H_v, a.scale, a.state_idx, a.P, order + a.N + 1);
     return hipGetLastError();
+}
+
+// The kernel instantiated for the requested prologue (none: the plain kernel).
+template <int NS, int NVT, int NO>
+static hipError_t launch_pipe(const PrefillArgs& a, int32_t* order, hipStream_t stream) {
+    switch (a.flags & (kFlagQkL2Norm | kFlagGateLogits)) {
+        case kFlagQkL2Norm: return launch_pipe_pro<NS, NVT, NO, kFlagQkL2Norm>(a, order, stream);
+        case kFlagGateLogits: return launch_pipe_pro<NS, NVT, NO, kFlagGateLogits>(a, order, stream);
+        case kFlagQkL2Norm | kFlagGateLogits:
+            return launch_pipe_pro<NS, NVT, NO, kFlagQkL2Norm | kFlagGateLogits>(a, order, stream);
+        default: return launch_pipe_pro<NS, NVT, NO, 0>(a, order, stream);
+    }
 }
 
 // One workgroup per (sequence, head) when there are enough of them to fill the

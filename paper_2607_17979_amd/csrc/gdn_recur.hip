@@ -61,7 +61,7 @@ __global__ __launch_bounds__(256) void prefill_recur_kernel(
     const float* __restrict__ g, const float* __restrict__ beta, const int32_t* __restrict__ cu,
     int32_t* __restrict__ order, const float* initial_state, float* final_state,
     uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale,
-    const int32_t* __restrict__ state_idx, int P, int short_only) {
+    const int32_t* __restrict__ state_idx, int P, int short_only, int flags) {
     __shared__ Smem sm;
     __shared__ int nlong;
     if (blockIdx.x == 0) {
@@ -126,9 +126,14 @@ __global__ __launch_bounds__(256) void prefill_recur_kernel(
         // stage the tokens: 16 segments of 8 values per k or q row, 4 per v slice
         if (tid < len * (D / 8)) {
             const int t = tid / (D / 8), seg = tid - t * (D / 8);
-            const size_t src = (size_t)(t0 + t) * qk_stride + (size_t)hq * D + seg * 8;
-            const uint4 kk = *reinterpret_cast<const uint4*>(k + src);
-            const uint4 qq = *reinterpret_cast<const uint4*>(q + src);
+            const size_t row = (size_t)(t0 + t) * qk_stride + (size_t)hq * D;
+            const size_t src = row + seg * 8;
+            uint4 kk = *reinterpret_cast<const uint4*>(k + src);
+            uint4 qq = *reinterpret_cast<const uint4*>(q + src);
+            if (flags & kFlagQkL2Norm) {
+                kk = scale_bf16x8(kk, row_inv_norm<D>(k + row));
+                qq = scale_bf16x8(qq, row_inv_norm<D>(q + row));
+            }
             const uint32_t kw[4] = {kk.x, kk.y, kk.z, kk.w}, qw[4] = {qq.x, qq.y, qq.z, qq.w};
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -144,8 +149,10 @@ __global__ __launch_bounds__(256) void prefill_recur_kernel(
                 *reinterpret_cast<const uint4*>(v + (size_t)(t0 + t) * v_stride + (size_t)h * D + row0 + seg * 8);
         }
         if (tid < len) {
-            sm.tok.alpha[tid] = fast_exp(g[(size_t)(t0 + tid) * H_v + h]);
-            sm.tok.b[tid] = beta[(size_t)(t0 + tid) * H_v + h];
+            const float gi = g[(size_t)(t0 + tid) * H_v + h], bi = beta[(size_t)(t0 + tid) * H_v + h];
+            const bool logits = (flags & kFlagGateLogits) != 0;
+            sm.tok.alpha[tid] = fast_exp(logits ? gate_from_logit(gi) : gi);
+            sm.tok.b[tid] = logits ? beta_from_logit(bi) : bi;
         }
         __syncthreads();
         // k . q per token, summed in the row layout below (8 tokens per wave)
@@ -216,7 +223,7 @@ hipError_t launch_prefill_recur(const PrefillArgs& a, int32_t* order, hipStream_
     hipLaunchKernelGGL(recur::prefill_recur_kernel, dim3((unsigned)grid), dim3(64 * recur::NWAVE), 0, stream,
                        (const uint16_t*)a.q, (const uint16_t*)a.k, (const uint16_t*)a.v, a.g, a.beta,
                        a.cu_seqlens, order, a.initial_state, a.final_state, (uint16_t*)a.o, a.N, a.H_qk,
-                       a.H_v, a.scale, a.state_idx, a.P, a.short_only ? 1 : 0);
+                       a.H_v, a.scale, a.state_idx, a.P, a.short_only ? 1 : 0, a.flags);
     return hipGetLastError();
 }
 

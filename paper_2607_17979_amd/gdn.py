@@ -26,13 +26,24 @@ __all__ = [
     "gdn_prefill_varlen_indexed",
     "gdn_decode_multitoken",
     "gdn_prefill_varlen_noalloc",
+    "gdn_decode_ex",
+    "gdn_prefill_varlen_ex",
+    "GDN_QK_L2NORM",
+    "GDN_GATE_LOGITS",
+    "GDN_SHORT_ONLY",
     "workspace_fault",
     "EXPORTED_SYMBOLS",
 ]
 
 EXPORTED_SYMBOLS = ("gdn_last_error", "gdn_abi_version", "gdn_decode", "gdn_decode_indexed",
                     "gdn_prefill_workspace_size", "gdn_prefill_varlen", "gdn_prefill_varlen_indexed",
-                    "gdn_decode_multitoken", "gdn_prefill_varlen_noalloc")
+                    "gdn_decode_multitoken", "gdn_prefill_varlen_noalloc", "gdn_decode_ex",
+                    "gdn_prefill_varlen_ex")
+
+# flag bits of the _ex entry points (enum gdn_flags in include/gdn.h)
+GDN_QK_L2NORM = 1
+GDN_GATE_LOGITS = 2
+GDN_SHORT_ONLY = 4
 
 _STATUS = {0: "GDN_OK", -1: "GDN_EINVAL", -2: "GDN_EUNSUPPORTED", -3: "GDN_EALIGN",
            -4: "GDN_EWORKSPACE", -5: "GDN_EHIP"}
@@ -79,6 +90,11 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.gdn_prefill_varlen_noalloc.restype = ci
     lib.gdn_prefill_varlen_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                                ci, ci, ci, ci, ci, ci, ci, cf, vp]
+    lib.gdn_decode_ex.restype = ci
+    lib.gdn_decode_ex.argtypes = [vp, vp, vp, vp, vp, vp, vp, ci, vp, ci, ci, ci, ci, ci, cf, ci, vp]
+    lib.gdn_prefill_varlen_ex.restype = ci
+    lib.gdn_prefill_varlen_ex.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, ci, vp,
+                                          ci, ci, ci, ci, ci, ci, ci, cf, ci, vp, sz, vp]
     lib.gdn_decode_multitoken.restype = ci
     lib.gdn_decode_multitoken.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp,
                                           ci, ci, ci, ci, ci, ci, cf, vp, sz, vp]
@@ -361,3 +377,78 @@ def gdn_prefill_varlen_noalloc(q, k, v, g, beta, cu_seqlens, initial_state, fina
                                           _ptr(cu_seqlens), _ptr(initial_state), _ptr(final_state),
                                           _ptr(o), N, T, H_qk, H_v, D, D, chunk, float(scale),
                                           _stream(q, stream)))
+
+
+def gdn_decode_ex(q, k, v, g, beta, state, o, state_idx=None, flags: int = 0, scale: float = 1.0,
+                  stream=None) -> None:
+    """gdn_decode / gdn_decode_indexed with the fused input prologue (see
+    include/gdn.h): ``flags`` GDN_QK_L2NORM (q, k normalised in the kernel)
+    and/or GDN_GATE_LOGITS (g, beta hold logits).  ``state_idx`` (int32 [B])
+    makes ``state`` a pool of slots."""
+    import torch
+
+    B, H_qk, D = q.shape
+    H_v = v.shape[1]
+    dev = q.device
+    if dev.type != "cuda":
+        raise ValueError("tensors must be on a GPU device")
+    _need(q, "q", torch.bfloat16, (B, H_qk, D), dev)
+    _need(k, "k", torch.bfloat16, (B, H_qk, D), dev)
+    _need(v, "v", torch.bfloat16, (B, H_v, D), dev)
+    _need(g, "g", torch.float32, (B, H_v), dev)
+    _need(beta, "beta", torch.float32, (B, H_v), dev)
+    P = 0
+    if state_idx is None:
+        _need(state, "state", torch.float32, (B, H_v, D, D), dev)
+    else:
+        P = state.shape[0]
+        _need(state, "state", torch.float32, (P, H_v, D, D), dev)
+        _need(state_idx, "state_idx", torch.int32, (B,), dev)
+    _need(o, "o", torch.bfloat16, (B, H_v, D), dev)
+    lib = load_library()
+    _check(lib.gdn_decode_ex(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(state), _ptr(state_idx),
+                             P, _ptr(o), B, H_qk, H_v, D, D, float(scale), int(flags), _stream(q, stream)))
+
+
+def gdn_prefill_varlen_ex(q, k, v, g, beta, cu_seqlens, initial_state, final_state, o, state_idx=None,
+                          flags: int = 0, scale: float = 1.0, chunk: Optional[int] = None, workspace=None,
+                          stream=None):
+    """gdn_prefill_varlen / gdn_prefill_varlen_indexed / gdn_decode_multitoken
+    with the fused input prologue (see include/gdn.h).  ``state_idx`` (int32
+    [N]) makes ``final_state`` a pool of slots updated in place;
+    GDN_SHORT_ONLY in ``flags`` takes the multi-token decode route.  Returns
+    the workspace."""
+    import torch
+
+    T, H_qk, D = q.shape
+    H_v = v.shape[1]
+    N = cu_seqlens.shape[0] - 1
+    dev = q.device
+    if dev.type != "cuda":
+        raise ValueError("tensors must be on a GPU device")
+    _need(q, "q", torch.bfloat16, (T, H_qk, D), dev)
+    _need(k, "k", torch.bfloat16, (T, H_qk, D), dev)
+    _need(v, "v", torch.bfloat16, (T, H_v, D), dev)
+    _need(g, "g", torch.float32, (T, H_v), dev)
+    _need(beta, "beta", torch.float32, (T, H_v), dev)
+    _need(cu_seqlens, "cu_seqlens", torch.int32, (N + 1,), dev)
+    P = 0
+    if state_idx is None:
+        if initial_state is not None:
+            _need(initial_state, "initial_state", torch.float32, (N, H_v, D, D), dev)
+        _need(final_state, "final_state", torch.float32, (N, H_v, D, D), dev)
+    else:
+        P = final_state.shape[0]
+        _need(final_state, "final_state", torch.float32, (P, H_v, D, D), dev)
+        _need(state_idx, "state_idx", torch.int32, (N,), dev)
+    _need(o, "o", torch.bfloat16, (T, H_v, D), dev)
+    chunk = default_chunk(D) if chunk is None else chunk
+    need = gdn_prefill_workspace_size(N, T, H_v, D, D, chunk)
+    workspace = _workspace_for(q, need, workspace, stream)
+    lib = load_library()
+    _check(lib.gdn_prefill_varlen_ex(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(cu_seqlens),
+                                     _ptr(initial_state), _ptr(final_state), _ptr(state_idx), P, _ptr(o),
+                                     N, T, H_qk, H_v, D, D, chunk, float(scale), int(flags),
+                                     _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                     _stream(q, stream)))
+    return workspace

@@ -144,10 +144,10 @@ class PrefillInputs:
 
 def decode_inputs(seed: int, B: int, H_qk: int, H_v: int, D: int,
                   state_std: float = 0.02, scale: float = 1.0,
-                  qkv_dtype: str = "bf16") -> DecodeInputs:
+                  qkv_dtype: str = "bf16", raw: Optional[float] = None) -> DecodeInputs:
     """Draw one decode step and its prior state.  ``qkv_dtype="f32"`` keeps
-    q/k/v as fp32 (oracle-only use)."""
-    step = decode_step_inputs(seed, 0, B, H_qk, H_v, D, qkv_dtype=qkv_dtype)
+    q/k/v as fp32 (oracle-only use); ``raw`` as decode_step_inputs."""
+    step = decode_step_inputs(seed, 0, B, H_qk, H_v, D, qkv_dtype=qkv_dtype, raw=raw)
     step.state = decode_state(seed, B, H_v, D, state_std)
     step.scale = scale
     return step
@@ -161,15 +161,23 @@ def decode_state(seed: int, B: int, H_v: int, D: int, state_std: float = 0.02) -
 
 
 def decode_step_inputs(seed: int, step: int, B: int, H_qk: int, H_v: int, D: int,
-                       qkv_dtype: str = "bf16") -> DecodeInputs:
-    """Fresh q, k, v, g, beta for decode step ``step`` (state left as None)."""
+                       qkv_dtype: str = "bf16", raw: Optional[float] = None) -> DecodeInputs:
+    """Fresh q, k, v, g, beta for decode step ``step`` (state left as None).
+    ``raw`` (a scale) draws the inputs of the fused prologue instead: q, k
+    N(0, raw^2) per element, not normalised; g and beta the N(0, 1) logits
+    themselves (g = -softplus and beta = sigmoid of them are then the
+    kernel's work)."""
     bf = qkv_dtype == "bf16"
-    q = _normal((seed, step, _Q), (B, H_qk, D), unit_last=True, bf16=bf)
-    k = _normal((seed, step, _K), (B, H_qk, D), unit_last=True, bf16=bf)
+    unit = raw is None
+    std = 1.0 if raw is None else raw
+    q = _normal((seed, step, _Q), (B, H_qk, D), unit_last=unit, std=std, bf16=bf)
+    k = _normal((seed, step, _K), (B, H_qk, D), unit_last=unit, std=std, bf16=bf)
     v = _normal((seed, step, _V), (B, H_v, D), bf16=bf)
-    beta = _sigmoid(_normal((seed, step, _BETA), (B, H_v)))
-    g = -_softplus(_normal((seed, step, _G), (B, H_v)))
-    return DecodeInputs(q, k, v, g, beta, None)
+    xb = _normal((seed, step, _BETA), (B, H_v))
+    xg = _normal((seed, step, _G), (B, H_v))
+    if raw is not None:
+        return DecodeInputs(q, k, v, xg, xb, None)
+    return DecodeInputs(q, k, v, -_softplus(xg), _sigmoid(xb), None)
 
 
 def varlen_lengths(seed: int, N: int, lo: int, hi: int) -> np.ndarray:
@@ -180,20 +188,25 @@ def varlen_lengths(seed: int, N: int, lo: int, hi: int) -> np.ndarray:
 
 def prefill_inputs(seed: int, lengths: Sequence[int], H_qk: int, H_v: int, D: int,
                    state_std: Optional[float] = None, scale: float = 1.0,
-                   qkv_dtype: str = "bf16") -> PrefillInputs:
+                   qkv_dtype: str = "bf16", raw: Optional[float] = None) -> PrefillInputs:
     """Draw a packed varlen batch.  ``state_std=None`` means a zero initial state
-    (passed to the library as NULL)."""
+    (passed to the library as NULL).  ``raw`` (a scale) draws the inputs of the
+    fused prologue instead: q, k N(0, raw^2) per element, not normalised; g and
+    beta the N(0, 1) logits themselves."""
     lengths = np.asarray(lengths, dtype=np.int64)
     N = len(lengths)
     cu = np.zeros(N + 1, np.int64)
     np.cumsum(lengths, out=cu[1:])
     T = int(cu[-1])
     bf = qkv_dtype == "bf16"
-    q = _normal((seed, _Q), (T, H_qk, D), unit_last=True, bf16=bf)
-    k = _normal((seed, _K), (T, H_qk, D), unit_last=True, bf16=bf)
+    unit = raw is None
+    std = 1.0 if raw is None else raw
+    q = _normal((seed, _Q), (T, H_qk, D), unit_last=unit, std=std, bf16=bf)
+    k = _normal((seed, _K), (T, H_qk, D), unit_last=unit, std=std, bf16=bf)
     v = _normal((seed, _V), (T, H_v, D), bf16=bf)
-    beta = _sigmoid(_normal((seed, _BETA), (T, H_v)))
-    g = -_softplus(_normal((seed, _G), (T, H_v)))
+    xb = _normal((seed, _BETA), (T, H_v))
+    xg = _normal((seed, _G), (T, H_v))
+    beta, g = (xb, xg) if raw is not None else (_sigmoid(xb), -_softplus(xg))
     init = None
     if state_std is not None:
         init = _normal((seed, _STATE), (N, H_v, D, D), std=state_std)

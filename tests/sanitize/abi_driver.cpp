@@ -63,6 +63,15 @@ int main() {
             st = gdn_prefill_varlen_noalloc(P(0), P(1), P(2), (const float*)P(3), (const float*)P(4),
                                             (const int32_t*)P(5), (const float*)P(6), (float*)P(7), P(8), I(9),
                                             I(10), I(11), I(12), I(13), I(14), I(15), F(16), P(17));
+        } else if (fn == "gdn_decode_ex") {
+            st = gdn_decode_ex(P(0), P(1), P(2), (const float*)P(3), (const float*)P(4), (float*)P(5),
+                               (const int32_t*)P(6), I(7), P(8), I(9), I(10), I(11), I(12), I(13), F(14), I(15),
+                               P(16));
+        } else if (fn == "gdn_prefill_varlen_ex") {
+            st = gdn_prefill_varlen_ex(P(0), P(1), P(2), (const float*)P(3), (const float*)P(4),
+                                       (const int32_t*)P(5), (const float*)P(6), (float*)P(7),
+                                       (const int32_t*)P(8), I(9), P(10), I(11), I(12), I(13), I(14), I(15),
+                                       I(16), I(17), F(18), I(19), P(20), Z(21), P(22));
         } else if (fn == "gdn_abi_version") {
             st = gdn_abi_version();
         } else {

@@ -42,7 +42,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert lib.gdn_abi_version() == 200
+    assert lib.gdn_abi_version() == 210
 
 
 def decode(lib, q=P, k=P, v=P, g=P, beta=P, state=P, o=P, B=2, H_qk=1, H_v=2, Dk=128, Dv=128,
@@ -255,3 +255,43 @@ def test_prefill_noalloc_rejects(lib, kw, status, msg):
 
 def test_prefill_noalloc_zero_sequences_is_noop(lib):
     assert noalloc(lib, q=None, k=None, v=None, g=None, beta=None, cu=None, fin=None, o=None, N=0, T=0) == OK
+
+
+def decode_ex(lib, q=P, k=P, v=P, g=P, beta=P, state=P, idx=None, Pn=0, o=P, B=2, H_qk=1, H_v=2, Dk=128,
+              Dv=128, scale=1.0, flags=0):
+    return lib.gdn_decode_ex(q, k, v, g, beta, state, idx, Pn, o, B, H_qk, H_v, Dk, Dv, scale, flags, None)
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(flags=4), EINVAL, "flags 0x4"),
+    (dict(flags=8), EINVAL, "flags 0x8"),
+    (dict(B=-1, flags=3), EINVAL, "B must be"),
+    (dict(state=None, flags=1), EINVAL, "state is NULL"),
+    (dict(idx=P, Pn=-1, flags=2), EINVAL, "P must be"),
+    (dict(idx=P + 2, Pn=4), EALIGN, "state_idx"),
+])
+def test_decode_ex_rejects(lib, kw, status, msg):
+    assert decode_ex(lib, **kw) == status
+    assert msg in gdn.gdn_last_error()
+
+
+def prefill_ex(lib, q=P, k=P, v=P, g=P, beta=P, cu=P, init=None, fin=P, idx=None, Pn=0, o=P, N=3, T=10,
+               H_qk=1, H_v=2, Dk=128, Dv=128, chunk=64, flags=0, ws=P, ws_bytes=256):
+    return lib.gdn_prefill_varlen_ex(q, k, v, g, beta, cu, init, fin, idx, Pn, o, N, T, H_qk, H_v, Dk, Dv, chunk,
+                                     1.0, flags, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(flags=8), EINVAL, "flags 0x8"),
+    (dict(idx=P, Pn=4, init=P + 0x100000), EINVAL, "in place"),
+    (dict(flags=4, init=P + 0x100000), EINVAL, "in place"),
+    (dict(flags=4, Dk=16, Dv=16, chunk=16), EUNSUP, "head dim 128"),
+    (dict(flags=4, chunk=16), EUNSUP, "use 64"),
+    (dict(flags=4, T=25), EINVAL, "more than 8 tokens"),
+    (dict(flags=3, chunk=32), EUNSUP, "chunk 32"),
+    (dict(idx=P + 1, Pn=4, flags=1), EALIGN, "state_idx"),
+    (dict(flags=1, ws=None), EWS, "workspace"),
+])
+def test_prefill_ex_rejects(lib, kw, status, msg):
+    assert prefill_ex(lib, **kw) == status
+    assert msg in gdn.gdn_last_error()

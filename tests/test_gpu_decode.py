@@ -25,7 +25,7 @@ def test_library_is_the_native_one():
 
     dev = device()
     lib = gdn.load_library()
-    assert lib.gdn_abi_version() == 200
+    assert lib.gdn_abi_version() == 210
     maps = open("/proc/self/maps").read()
     assert "libgdn_mi355x.so" in maps
     assert torch.cuda.get_device_properties(dev).gcnArchName.startswith("gfx950")

@@ -83,7 +83,8 @@ def _cases():
     of test_abi_host.py, plus calls that pass the checks."""
     tables = [(abi.decode, abi.test_decode_rejects), (abi.decode_indexed, abi.test_decode_indexed_rejects),
               (abi.prefill, abi.test_prefill_rejects), (abi.prefill_indexed, abi.test_prefill_indexed_rejects),
-              (abi.multitoken, abi.test_decode_multitoken_rejects)]
+              (abi.multitoken, abi.test_decode_multitoken_rejects), (abi.decode_ex, abi.test_decode_ex_rejects),
+              (abi.prefill_ex, abi.test_prefill_ex_rejects)]
     cases = []
     for helper, test in tables:
         params = [m for m in test.pytestmark if m.name == "parametrize"][0].args[1]
