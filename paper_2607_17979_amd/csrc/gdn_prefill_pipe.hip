@@ -108,12 +108,55 @@ struct Smem {
     alignas(16) float rn[NP][2][C];   // per producer, with the q/k L2 norm: 1 / |row| of its K, Q rows
 };
 
-// Inclusive prefix sum over the 64 lanes of a wave (DPP row shifts, then row
-// broadcasts across the four rows of 16 lanes).
 template <int CTRL, int ROWMASK, bool BOUND>
 __device__ __forceinline__ float dpp_src(float x) {
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, ROWMASK, 0xF, BOUND));
 }
+// Terms of one row of the diagonal-block solve: acc + sum_i n_i(R) y_i over
+// the CNT (1 to 4) elements of n and y in order, where n_i(R) is n_i in lane R
+// of this lane's row of 16 lanes: v_fmac_f32 with a DPP row broadcast
+// (row_newbcast, gfx90a and later) on n_i, one instruction per term.  The
+// block starts with two wait states, so the DPP reads are safe even if the
+// compiler has just written n's registers with a vector instruction.
+template <int R, int CNT>
+__device__ __forceinline__ float fmac_bcast(float acc, const f32x4_t& n, const float* y) {
+    static_assert(R >= 1 && R < 16 && CNT >= 1 && CNT <= 4, "lane and term count");
+    if constexpr (CNT == 4)
+        asm("s_nop 1\n"
+            "v_fmac_f32_dpp %0, %1, %5 row_newbcast:%9 row_mask:0xf bank_mask:0xf\n"
+            "v_fmac_f32_dpp %0, %2, %6 row_newbcast:%9 row_mask:0xf bank_mask:0xf\n"
+            "v_fmac_f32_dpp %0, %3, %7 row_newbcast:%9 row_mask:0xf bank_mask:0xf\n"
+            "v_fmac_f32_dpp %0, %4, %8 row_newbcast:%9 row_mask:0xf bank_mask:0xf"
+            : "+v"(acc)
+            : "v"(n[0]), "v"(n[1]), "v"(n[2]), "v"(n[3]), "v"(y[0]), "v"(y[1]), "v"(y[2]), "v"(y[3]), "i"(R));
+    else if constexpr (CNT == 3)
+        asm("s_nop 1\n"
+            "v_fmac_f32_dpp %0, %1, %4 row_newbcast:%7 row_mask:0xf bank_mask:0xf\n"
+            "v_fmac_f32_dpp %0, %2, %5 row_newbcast:%7 row_mask:0xf bank_mask:0xf\n"
+            "v_fmac_f32_dpp %0, %3, %6 row_newbcast:%7 row_mask:0xf bank_mask:0xf"
+            : "+v"(acc) : "v"(n[0]), "v"(n[1]), "v"(n[2]), "v"(y[0]), "v"(y[1]), "v"(y[2]), "i"(R));
+    else if constexpr (CNT == 2)
+        asm("s_nop 1\n"
+            "v_fmac_f32_dpp %0, %1, %3 row_newbcast:%5 row_mask:0xf bank_mask:0xf\n"
+            "v_fmac_f32_dpp %0, %2, %4 row_newbcast:%5 row_mask:0xf bank_mask:0xf"
+            : "+v"(acc) : "v"(n[0]), "v"(n[1]), "v"(y[0]), "v"(y[1]), "i"(R));
+    else
+        asm("s_nop 1\n"
+            "v_fmac_f32_dpp %0, %1, %2 row_newbcast:%3 row_mask:0xf bank_mask:0xf"
+            : "+v"(acc) : "v"(n[0]), "v"(y[0]), "i"(R));
+    return acc;
+}
+// Row R of the solve: acc + sum_{i < R} nrow_i(R) xs_i, terms in order of i.
+template <int R>
+__device__ __forceinline__ float fsolve_row(const f32x4_t (&nrow)[4], const float (&xs)[16], float acc) {
+    acc = fmac_bcast<R, (R < 4 ? R : 4)>(acc, nrow[0], &xs[0]);
+    if constexpr (R > 4) acc = fmac_bcast<R, (R - 4 < 4 ? R - 4 : 4)>(acc, nrow[1], &xs[4]);
+    if constexpr (R > 8) acc = fmac_bcast<R, (R - 8 < 4 ? R - 8 : 4)>(acc, nrow[2], &xs[8]);
+    if constexpr (R > 12) acc = fmac_bcast<R, R - 12>(acc, nrow[3], &xs[12]);
+    return acc;
+}
+// Inclusive prefix sum over the 64 lanes of a wave (DPP row shifts, then row
+// broadcasts across the four rows of 16 lanes).
 __device__ __forceinline__ float wave_prefix_sum(float x) {
     x += dpp_src<0x111, 0xF, true>(x);  // row_shr:1
     x += dpp_src<0x112, 0xF, true>(x);  // row_shr:2
@@ -379,7 +422,7 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
         }
     }
     // ---- A = beta_r exp(gamma_r - gamma_c) (K K^T)_rc, c < r.
-    //      Diagonal blocks: acc(N_b^T) from the (symmetric) Gram tile;
+    //      Diagonal blocks: acc(-N_b^T) from the (symmetric) Gram tile;
     //      below the diagonal: acc(A_bk^T).
     f32x4_t nt[NCT], at[NBLK];
 #pragma unroll
@@ -390,7 +433,7 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
         const f32x4_t gc = *reinterpret_cast<const f32x4_t*>(&gam[16 * b + 4 * gq]);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-            nt[b][i] = (4 * gq + i < m) ? br[b] * fast_exp(gr[b] - gc[i]) * acc[i] : 0.f;
+            nt[b][i] = (4 * gq + i < m) ? -(br[b] * fast_exp(gr[b] - gc[i]) * acc[i]) : 0.f;
 #pragma unroll
         for (int kb = 0; kb < b; ++kb) {
             f32x4_t ag = {0.f, 0.f, 0.f, 0.f};
@@ -402,34 +445,27 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
         }
     }
     // ---- T = (I + A)^-1: diagonal blocks D_b = (I + N_b)^-1 by forward
-    //      substitution in fp32, lane 16 b + j solving column j of
-    //      block b (rows of N_b are read as LDS broadcasts); then block
-    //      columns T_bJ = -D_b sum_{kb=J}^{b-1} A_{b,kb} T_{kb,J} (b > J)
-    //      on split-bf16 MFMA.
+    //      substitution in fp32, lane 16 b + j solving column j of block b;
+    //      then block columns T_bJ = -D_b sum_{kb=J}^{b-1} A_{b,kb} T_{kb,J}
+    //      (b > J) on split-bf16 MFMA.
+    // Lane 16 b + m holds row m of -N_b in registers (through the scratch
+    // block, which transposes the accumulator layout); the solve takes
+    // element i of row r from lane 16 b + r with a DPP row broadcast, so its
+    // 120 multiply-adds wait on no LDS access.
     float* scb = scr + gq * SBS;  // this lane's block b = gq
 #pragma unroll
-    for (int b = 0; b < NCT; ++b)     // row m of N_b, columns 4 gq .. 4 gq + 3
+    for (int b = 0; b < NCT; ++b)     // row m of -N_b, columns 4 gq .. 4 gq + 3
         *reinterpret_cast<f32x4_t*>(&scr[b * SBS + m * SP + 4 * gq]) = nt[b];
-    // Row r + 1 of N_b is read while row r is solved; the scheduling
-    // fences keep the reads from being hoisted all at once.
+    f32x4_t nrow[4];
+#pragma unroll
+    for (int i4 = 0; i4 < 4; ++i4) nrow[i4] = *reinterpret_cast<const f32x4_t*>(&scb[m * SP + 4 * i4]);
     float xs[16];
-    f32x4_t nrow[2][4];
     xs[0] = (m == 0) ? 1.f : 0.f;
-    nrow[1][0] = *reinterpret_cast<const f32x4_t*>(&scb[1 * SP]);
-#pragma unroll
-    for (int r = 1; r < 16; ++r) {
-        const int cur = r & 1;
-        if (r + 1 < 16) {
-#pragma unroll
-            for (int i4 = 0; i4 < r + 1; i4 += 4)
-                nrow[cur ^ 1][i4 / 4] = *reinterpret_cast<const f32x4_t*>(&scb[(r + 1) * SP + i4]);
-        }
-        float acc = (r == m) ? 1.f : 0.f;
-#pragma unroll
-        for (int i = 0; i < r; ++i) acc = fmaf(-nrow[cur][i / 4][i % 4], xs[i], acc);
-        xs[r] = acc;
-        __builtin_amdgcn_sched_barrier(0);
-    }
+#define GDN_SOLVE_ROW(R) xs[R] = fsolve_row<R>(nrow, xs, (R == m) ? 1.f : 0.f);
+    GDN_SOLVE_ROW(1) GDN_SOLVE_ROW(2) GDN_SOLVE_ROW(3) GDN_SOLVE_ROW(4) GDN_SOLVE_ROW(5)
+    GDN_SOLVE_ROW(6) GDN_SOLVE_ROW(7) GDN_SOLVE_ROW(8) GDN_SOLVE_ROW(9) GDN_SOLVE_ROW(10)
+    GDN_SOLVE_ROW(11) GDN_SOLVE_ROW(12) GDN_SOLVE_ROW(13) GDN_SOLVE_ROW(14) GDN_SOLVE_ROW(15)
+#undef GDN_SOLVE_ROW
 #pragma unroll
     for (int r4 = 0; r4 < 16; r4 += 4)  // row m of the scratch block = column m of D_b
         *reinterpret_cast<f32x4_t*>(&scb[m * SP + r4]) = f32x4_t{xs[r4], xs[r4 + 1], xs[r4 + 2], xs[r4 + 3]};
