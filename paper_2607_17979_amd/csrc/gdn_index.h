@@ -41,8 +41,8 @@ __host__ __device__ inline int longest_first_rank(const int* len, int N, int i) 
 }
 
 // ---- token-by-token kernel: units (sequence n, value head h, row block blk),
-// u = (n H_v + h) BPH + blk, walked by workgroup w (w >= 1) as w - 1,
-// w - 1 + stride, ...
+// u = (n H_v + h) BPH + blk.  Workgroup w (w >= 1) walks the slots w - 1,
+// w - 1 + stride, ... and slot s holds unit recur_slot_unit(s).
 
 // Whether unit u runs in the token-by-token kernel: its sequence has at most
 // recur_max tokens and its state lies inside the pool (with state_idx).
@@ -57,13 +57,28 @@ __host__ __device__ inline bool recur_unit_runs(long u, int bph, int H_v, const 
     return true;
 }
 
-// The first unit at or after u (stepping by stride) that runs here, or a
-// value >= units.
-__host__ __device__ inline long recur_next_unit(long u, long stride, long units, int bph, int H_v,
+// Unit of slot s.  The grp consecutive units grp j .. grp j + grp - 1 (the
+// units that read the same q/k rows: the row blocks of the value heads of one
+// q/k head) sit in slots 8 apart; with a stride that is a multiple of 8 (or a
+// single pass) they run on workgroups 8 apart, which the dispatcher places on
+// one XCD, so those reads share its L2.  A last partial block of 8 grp slots
+// keeps the identity.  A bijection of [0, units).
+__host__ __device__ inline long recur_slot_unit(long s, long units, int grp) {
+    const long G = 8L * grp;
+    const long blk = s / G;
+    if (blk * G + G > units) return s;
+    const long r = s - blk * G;
+    return blk * G + grp * (r & 7) + (r >> 3);
+}
+
+// The first slot at or after s (stepping by stride) whose unit runs here, or
+// a value >= units.
+__host__ __device__ inline long recur_next_slot(long s, long stride, long units, int grp, int bph, int H_v,
                                                 const int32_t* cu, const int32_t* state_idx, int P,
                                                 int recur_max) {
-    while (u < units && !recur_unit_runs(u, bph, H_v, cu, state_idx, P, recur_max)) u += stride;
-    return u;
+    while (s < units && !recur_unit_runs(recur_slot_unit(s, units, grp), bph, H_v, cu, state_idx, P, recur_max))
+        s += stride;
+    return s;
 }
 
 // Fields of a unit that runs: its head, q/k head, row block, tokens and state

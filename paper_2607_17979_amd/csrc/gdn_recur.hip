@@ -89,16 +89,20 @@ __global__ __launch_bounds__(256) void prefill_recur_kernel(
     const int sub = lane / LPR, c = lane % LPR;
     const long units = (long)N * H_v * BPH;
     const size_t qk_stride = (size_t)H_qk * D, v_stride = (size_t)H_v * D;
-    // Unit u runs here if its sequence has at most kRecurMax tokens and its
-    // state lies inside the pool; a workgroup walks units u, u + stride, ...
+    // A unit runs here if its sequence has at most kRecurMax tokens and its
+    // state lies inside the pool; a workgroup walks slots s, s + stride, ...
+    // (the units of one q/k head on one XCD).
     const long stride = gridDim.x - 1;
-    auto next_unit = [&](long u) -> long {
-        return recur_next_unit(u, stride, units, BPH, H_v, cu, state_idx, P, kRecurMax);
+    const int grp = (H_v / H_qk) * BPH;
+    auto next_unit = [&](long s) -> long {
+        return recur_next_slot(s, stride, units, grp, BPH, H_v, cu, state_idx, P, kRecurMax);
     };
-    // The fields of a unit that runs here: its state (state n, or pool slot
+    // The fields of the unit in slot s: its state (state n, or pool slot
     // state_idx[n]), head, row block and tokens.
     typedef RecurUnit Unit;
-    auto unit_at = [&](long u) -> Unit { return recur_unit_at(u, BPH, H_v, H_qk, cu, state_idx); };
+    auto unit_at = [&](long s) -> Unit {
+        return recur_unit_at(recur_slot_unit(s, units, grp), BPH, H_v, H_qk, cu, state_idx);
+    };
     auto state_row = [&](const Unit& x) {
         const int row = x.blk * ROWS + wave * ROWS_PER_WAVE + sub;
         return ((size_t)x.shead * D + row) * D;

@@ -20,11 +20,14 @@ constexpr int kBph = 4;       // workgroups (row blocks) per (sequence, head) in
 constexpr int kChunk = 64;
 
 // The earlier form of the walk, reconstructed: one function scans for the
-// next unit that runs and returns all of its fields.
-RecurUnit legacy_next(long u, long stride, long units, int H_v, int H_qk, const int32_t* cu,
+// next slot whose unit runs and returns all of its fields (s is left at that
+// slot).
+RecurUnit legacy_next(long& s, long stride, long units, int H_v, int H_qk, const int32_t* cu,
                       const int32_t* state_idx, int P) {
     RecurUnit r;
-    for (; u < units; u += stride) {
+    const int grp = (H_v / H_qk) * kBph;
+    for (; s < units; s += stride) {
+        const long u = recur_slot_unit(s, units, grp);
         const long head = u / kBph;
         const int n = (int)(head / H_v);
         r.h = (int)(head - (long)n * H_v);
@@ -75,15 +78,17 @@ int main() {
     const int32_t* sidx = use_idx ? idx.data() : nullptr;
     // token-by-token walk, as the kernel runs it: workgroups 1 .. grid - 1
     const long units = (long)N * H_v * kBph, stride = grid_recur - 1;
+    const int grp = (H_v / H_qk) * kBph;
     for (int b = 1; b < grid_recur; ++b) {
-        long u = recur_next_unit(b - 1, stride, units, kBph, H_v, cu.data(), sidx, P, kRecurMax);
-        while (u < units) {
-            const RecurUnit r = recur_unit_at(u, kBph, H_v, H_qk, cu.data(), sidx);
+        long s = recur_next_slot(b - 1, stride, units, grp, kBph, H_v, cu.data(), sidx, P, kRecurMax);
+        while (s < units) {
+            const RecurUnit r = recur_unit_at(recur_slot_unit(s, units, grp), kBph, H_v, H_qk, cu.data(), sidx);
             std::printf("recur %d %ld %d %d %d %ld %d %d\n", b, r.u, r.h, r.hq, r.blk, r.shead, r.t0, r.len);
-            u = recur_next_unit(u + stride, stride, units, kBph, H_v, cu.data(), sidx, P, kRecurMax);
+            s = recur_next_slot(s + stride, stride, units, grp, kBph, H_v, cu.data(), sidx, P, kRecurMax);
         }
-        for (RecurUnit r = legacy_next(b - 1, stride, units, H_v, H_qk, cu.data(), sidx, P); r.u < units;
-             r = legacy_next(r.u + stride, stride, units, H_v, H_qk, cu.data(), sidx, P))
+        long ls = b - 1;
+        for (RecurUnit r = legacy_next(ls, stride, units, H_v, H_qk, cu.data(), sidx, P); ls < units;
+             ls += stride, r = legacy_next(ls, stride, units, H_v, H_qk, cu.data(), sidx, P))
             std::printf("legacy %d %ld %d %d %d %ld %d %d\n", b, r.u, r.h, r.hq, r.blk, r.shead, r.t0, r.len);
     }
     // longest-first schedule (identity beyond kSortMax sequences)

@@ -128,16 +128,28 @@ def test_workspace_size_under_sanitizers(bins):
     assert got[5] == ((2147483000 + 2) * 4 + 255) // 256 * 256
 
 
+def _slot_unit(s, units, grp):
+    """Slot -> unit of the token-by-token walk: in each full block of 8 grp
+    slots, slots c, c + 8, c + 16, ... (one XCD) hold the grp units of one q/k
+    head; a last partial block is the identity."""
+    blk, r = divmod(s, 8 * grp)
+    if (blk + 1) * 8 * grp > units:
+        return s
+    return blk * 8 * grp + grp * (r % 8) + r // 8
+
+
 def _expected_recur(N, H_qk, H_v, P, grid, lengths, idx):
     """The unit walk of the token-by-token kernel, enumerated directly:
-    workgroup b >= 1 visits u = b - 1, b - 1 + (grid - 1), ... among the units
-    (sequence n, head h, row block blk) = u // (4 H_v), (u // 4) % H_v, u % 4
-    whose sequence has at most 8 tokens and whose slot is in the pool."""
+    workgroup b >= 1 visits slots b - 1, b - 1 + (grid - 1), ..., slot s holds
+    unit u = _slot_unit(s), and units are (sequence n, head h, row block blk) =
+    u // (4 H_v), (u // 4) % H_v, u % 4; only units whose sequence has at most
+    8 tokens and whose slot is in the pool run."""
     cu = np.concatenate([[0], np.cumsum(lengths)])
     units, stride, r = N * H_v * 4, grid - 1, H_v // H_qk
     out = []
     for b in range(1, grid):
-        for u in range(b - 1, units, stride):
+        for s in range(b - 1, units, stride):
+            u = _slot_unit(s, units, r * 4)
             n, h, blk = u // (4 * H_v), (u // 4) % H_v, u % 4
             if lengths[n] > 8:
                 continue
@@ -193,6 +205,16 @@ def test_work_walks_under_sanitizers(bins, seed):
         ok_slot = idx is None or 0 <= idx[n] < P
         assert nch == ((ln + 63) // 64 if (ln > 8 and ok_slot) else 0)
         assert slot == (n if idx is None else idx[n])
+    # the slot -> unit map is a bijection, and each workgroup's units of one
+    # q/k head sit on one XCD when the stride is a multiple of 8
+    for units in (1, 7, 31, 32, 33, 64, 100, 257, 1024):
+        for grp in (4, 8, 16):
+            assert sorted(_slot_unit(s, units, grp) for s in range(units)) == list(range(units))
+            full = units // (8 * grp) * 8 * grp
+            xcd = {}
+            for s in range(full):
+                xcd.setdefault(_slot_unit(s, units, grp) // grp, set()).add(s % 8)
+            assert all(len(v) == 1 for v in xcd.values())
     # logical_item is a bijection of [0, total)
     for key in ("logical2", "logical8"):
         by_total = {}
