@@ -331,24 +331,14 @@ __device__ __forceinline__ bf16x8_t row_frag(const uint16_t (*a)[PD], int r, int
 __device__ __forceinline__ uint4 ld16(const void* base, unsigned byte_off) {
     return *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(base) + byte_off);
 }
-// Streaming accesses, marked non-temporal so that they do not push out of L2
-// the K and Q rows that the producers read twice (operand fragments, then
-// staging a few chunks later): the V rows, read once, and the outputs.
+// Streaming load of the V rows (read once), marked non-temporal so that it
+// does not push out of L2 the K and Q rows that the producers read twice
+// (operand fragments, then staging a few chunks later).
 typedef unsigned u32x4v_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint4 ld16_stream(const void* base, unsigned byte_off) {
     const u32x4v_t r =
         __builtin_nontemporal_load(reinterpret_cast<const u32x4v_t*>(reinterpret_cast<const char*>(base) + byte_off));
     return uint4{r[0], r[1], r[2], r[3]};
-}
-// Output store: non-temporal when NT (each wave's stores cover 64 contiguous
-// bytes per token, two value tiles); with one tile (32 bytes per token and
-// store) non-temporal stores measured 7% slower on 2 x 65,536 tokens.
-template <bool NT>
-__device__ __forceinline__ void st16_out(uint16_t* p, const uint4& val) {
-    if constexpr (NT)
-        __builtin_nontemporal_store(u32x4v_t{val.x, val.y, val.z, val.w}, reinterpret_cast<u32x4v_t*>(p));
-    else
-        *reinterpret_cast<uint4*>(p) = val;
 }
 
 // Producer work for chunk lc of the work item described by pc, which is chunk
@@ -929,7 +919,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
                     const auto p1 = __builtin_amdgcn_permlane16_swap(cvt_pk(x[2], x[3]), cvt_pk(y[2], y[3]), false, false);
                     const uint4 pk = {p0[0], p1[0], p0[1], p1[1]};
                     if (row < L)
-                        st16_out<NVT % 2 == 0>(o + (size_t)(t0 + row) * v_stride + (size_t)h * D + vcol0 + col, pk);
+                        *reinterpret_cast<uint4*>(o + (size_t)(t0 + row) * v_stride + (size_t)h * D + vcol0 + col) = pk;
                 };
                 if constexpr (NVT % 2 == 0) {
 #pragma unroll
@@ -1035,7 +1025,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
                     const auto p1 = __builtin_amdgcn_permlane16_swap(cvt_pk(x[2], x[3]), cvt_pk(y[2], y[3]), false, false);
                     const uint4 pk = {p0[0], p1[0], p0[1], p1[1]};
                     if (row < L)
-                        st16_out<NVT % 2 == 0>(o + (size_t)(t0 + row) * v_stride + (size_t)it.h * D + vcol0 + col, pk);
+                        *reinterpret_cast<uint4*>(o + (size_t)(t0 + row) * v_stride + (size_t)it.h * D + vcol0 + col) = pk;
                 };
                 if constexpr (NVT % 2 == 0) {
 #pragma unroll
