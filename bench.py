@@ -245,9 +245,12 @@ def _settle(parts, seconds):
 
 def _time_parts(parts, steps, warmup, settle_s=0.0):
     """Settle the clocks (``settle_s`` seconds of untimed steps), run
-    ``warmup`` then ``steps`` steps of all parts in order; per-part HIP event
-    times on torch's current stream (the stream the library launches on) and
-    the wall time of the timed steps.  Returns (ms_per_step, [avg ms per part])."""
+    ``warmup`` then ``steps`` steps of all parts in order; HIP event times on
+    torch's current stream (the stream the library launches on) and the wall
+    time of the timed steps.  With one part, one event pair brackets all timed
+    steps (back-to-back launches, nothing recorded between them); with several,
+    each part of each step has its own pair, so that the parts can be told
+    apart.  Returns (ms_per_step, [avg ms per part])."""
     import torch
 
     if settle_s > 0:
@@ -256,6 +259,17 @@ def _time_parts(parts, steps, warmup, settle_s=0.0):
         for p in parts:
             p()
     torch.cuda.synchronize()
+    if len(parts) == 1:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        e0.record()
+        for _ in range(steps):
+            parts[0]()
+        e1.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        return wall * 1e3 / steps, [e0.elapsed_time(e1) / steps]
     evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
             for _ in parts] for _ in range(steps)]
     torch.cuda.synchronize()

@@ -378,6 +378,31 @@ def test_prefill_short_route_zero_initial_state():
     _full_oracle_check(inp, o, fin, "short route, zero state")
 
 
+@pytest.mark.parametrize("H_qk,H_v", [(4, 4), (2, 8)])
+def test_short_route_head_ratios(H_qk, H_v):
+    """The token-by-token walk groups the units that share a q/k head (the row
+    blocks of H_v / H_qk value heads) on one XCD; with 1 and 4 value heads per
+    q/k head (groups of 4 and 16 units, full and partial blocks of slots) every
+    unit still runs once: outputs and states against the oracle, and bit for
+    bit equal to the same call with q and k repeated per value head."""
+    import torch
+
+    dev = device()
+    rng = np.random.default_rng(49 + H_v)
+    lengths = [int(x) for x in rng.integers(0, 9, size=13)]
+    note(f"short route H_qk={H_qk} H_v={H_v} lengths={lengths}")
+    inp = wl.prefill_inputs(49 + H_v, lengths, H_qk, H_v, 128, state_std=0.02, scale=128 ** -0.5)
+    o, fin = _prefill_gpu(inp, dev)
+    _full_oracle_check(inp, o, fin, f"short route {H_qk}/{H_v}")
+    r = H_v // H_qk
+    rep = wl.PrefillInputs(np.repeat(inp.q, r, axis=1), np.repeat(inp.k, r, axis=1), inp.v, inp.g,
+                           inp.beta, inp.cu_seqlens, inp.initial_state, inp.scale)
+    o2, f2 = _prefill_gpu(rep, dev)
+    torch.cuda.synchronize()
+    assert torch.equal(o.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(fin, f2)
+
+
 def test_multi_token_decode_equals_decode_steps_bitwise():
     """B sequences with Tn new tokens each and states updated in place (a
     multi-token decode step) equal Tn gdn_decode calls bit for bit: the
