@@ -147,6 +147,17 @@ __device__ __forceinline__ typename Frag<K>::type acc_frag_hi(const f32x4_t& t0,
     }
 }
 
+// B operand, lo part, given the hi part from acc_frag_hi<32>: the same
+// residuals as acc_frag<32> (bf16 of x - hi for each element).
+__device__ __forceinline__ bf16x8_t acc_frag_lo32(const f32x4_t& t0, const f32x4_t& t1, const bf16x8_t& hi) {
+    const uint4 h = __builtin_bit_cast(uint4, hi);
+    const uint4 l = {cvt_pk(t0[0] - __uint_as_float(h.x << 16), t0[1] - __uint_as_float(h.x & 0xFFFF0000u)),
+                     cvt_pk(t0[2] - __uint_as_float(h.y << 16), t0[3] - __uint_as_float(h.y & 0xFFFF0000u)),
+                     cvt_pk(t1[0] - __uint_as_float(h.z << 16), t1[1] - __uint_as_float(h.z & 0xFFFF0000u)),
+                     cvt_pk(t1[2] - __uint_as_float(h.w << 16), t1[3] - __uint_as_float(h.w & 0xFFFF0000u))};
+    return __builtin_bit_cast(bf16x8_t, l);
+}
+
 // Round x to bf16 hi and the residual to lo (scalar form, for LDS stores).
 __device__ __forceinline__ void split_bf16(float x, uint16_t& hi, uint16_t& lo) {
     hi = f32_to_bf16(x);

@@ -58,6 +58,9 @@ constexpr int SP = 20;                      // row pitch (fp32) of the producers
 // lane groups, each reading a row of its own block, hit different banks.
 constexpr int SBS = 16 * SP + 4;
 constexpr int kSpinLimit = 1 << 20;
+// K S0^T takes the lo half of S0 only when the chunk's total decay
+// exp(gamma_last) exceeds this (see the state waves' first phase).
+constexpr float kS0LoDecay = 1.f / 16;
 
 __device__ __forceinline__ constexpr int bidx(int i, int j) { return i * (i + 1) / 2 + j; }
 
@@ -666,6 +669,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
         // (their LDS round trip overlaps that chunk's output stores); a wait
         // reads again only if the value seen was short.  0: nothing seen yet.
         unsigned seen_stg = 0, seen_hs = 0, seen_rdy = 0, seen_hu = 0;
+        float seen_egl = 0.f;  // the next chunk's exp(gamma_last), valid once seen_rdy says ready
         for (int pass = 0;; ++pass) {
         const int item = item_at(pass);
         if (item < 0) break;
@@ -700,25 +704,60 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
             wait_seen(&sm.cnt[CNT_STG], (unsigned)(xs + 1), seen_stg, fault);
             // with output waves: the previous chunk's S0 hi operands were read
             if constexpr (NO > 0) wait_seen(&sm.cnt[CNT_HAND0 + 4 * wave + 1], (unsigned)xs, seen_hs, fault);
-            // K S0^T (S0 hi + lo), rows t; (Q S0^T)^T (S0 hi), rows v, unless
-            // an output wave takes it (it gets the S0 hi operands instead)
+            // K S0^T (S0 hi + lo, or hi alone), rows t; (Q S0^T)^T (S0 hi), rows
+            // v, unless an output wave takes it (it gets the S0 hi operands
+            // instead).
+            // The lo half of S0 matters in K S0^T only while the state persists:
+            // every term of the chunk's new state that depends on S0 carries
+            // the chunk's total decay exp(gamma_last), so dropping S0 lo there
+            // changes the state by about 2^-9 exp(gamma_last) of its size per
+            // chunk, which later chunks decay further.  With exp(gamma_last) <=
+            // kS0LoDecay the product takes S0 hi alone (uniform branches around
+            // the lo split and products).  The decay comes from the chunk's
+            // result slot, which for stream chunks after the first is ready
+            // once the chunk is staged (a producer publishes before it
+            // stages); stream chunk 0 waits for it here.  The choice depends
+            // on the chunk's own gates only, never on the batch around it.
+            // (The decay was read with the ready counter at the end of the
+            // previous chunk; read again only if the slot was not ready then.)
+            bool s0lo;
+            {
+                const unsigned target = (unsigned)(xs / NP + 1);
+                float egl = seen_egl;
+                if (rdy_seen < target) {
+                    wait_ge(&sm.cnt[CNT_READY0 + xs % NP], target, fault);
+                    egl = sl.eg[C - 1];
+                }
+                s0lo = __builtin_amdgcn_readfirstlane((int)(egl > kS0LoDecay)) != 0;
+            }
             f32x4_t ks[NCT][NVT], ot[NVT][NCT];
             const f32x4_t zero4 = {0.f, 0.f, 0.f, 0.f};
             // Software pipeline over the contraction: the operand reads of step
             // kq + 1 are issued ahead of the products of step kq (the barrier
             // keeps the scheduler from sinking them towards their use), and
-            // the hi/lo split of step kq + 1 is interleaved with those products.
+            // the split of step kq + 1 is interleaved with those products.  The
+            // lo halves (split and products) sit in uniform branches of their
+            // own; each accumulator still takes hi then lo of every step.
             bf16x8_t ak[2][NCT], aq[2][NCT], bh[2][NVT], bl[2][NVT];
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) {
                 ak[0][ct] = row_frag(kb, 16 * ct + m, 0, gq);
                 if constexpr (NO == 0) aq[0][ct] = row_frag(sm.qb, 16 * ct + m, 0, gq);
             }
+            auto split_s0 = [&](int kq, int buf) {
 #pragma unroll
-            for (int vt = 0; vt < NVT; ++vt) {
-                acc_frag<32>(st[0][vt], st[1][vt], bh[0][vt], bl[0][vt]);
-                if constexpr (NO > 0) sm.hs[wave % (NO > 0 ? NO : 1)][0][vt][lane] = __builtin_bit_cast(uint4, bh[0][vt]);
-            }
+                for (int vt = 0; vt < NVT; ++vt) {
+                    bh[buf][vt] = acc_frag_hi<32>(st[2 * kq][vt], st[2 * kq + 1][vt]);
+                    if constexpr (NO > 0)
+                        sm.hs[wave % (NO > 0 ? NO : 1)][kq][vt][lane] = __builtin_bit_cast(uint4, bh[buf][vt]);
+                }
+                if (s0lo) {
+#pragma unroll
+                    for (int vt = 0; vt < NVT; ++vt)
+                        bl[buf][vt] = acc_frag_lo32(st[2 * kq][vt], st[2 * kq + 1][vt], bh[buf][vt]);
+                }
+            };
+            split_s0(0, 0);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int kq = 0; kq < D / 32; ++kq) {
@@ -731,34 +770,47 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
                     }
                 }
                 __builtin_amdgcn_sched_barrier(0);
-                if (kq + 1 < D / 32) {
-#pragma unroll
-                    for (int vt = 0; vt < NVT; ++vt) {
-                        acc_frag<32>(st[2 * kq + 2][vt], st[2 * kq + 3][vt], bh[cur ^ 1][vt], bl[cur ^ 1][vt]);
-                        if constexpr (NO > 0)
-                            sm.hs[wave % (NO > 0 ? NO : 1)][kq + 1][vt][lane] = __builtin_bit_cast(uint4, bh[cur ^ 1][vt]);
-                    }
-                }
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
                     for (int vt = 0; vt < NVT; ++vt) {
                         ks[ct][vt] = mma(ak[cur][ct], bh[cur][vt], kq == 0 ? zero4 : ks[ct][vt]);
-                        ks[ct][vt] = mma(ak[cur][ct], bl[cur][vt], ks[ct][vt]);
                         if constexpr (NO == 0) ot[vt][ct] = mma(bh[cur][vt], aq[cur][ct], kq == 0 ? zero4 : ot[vt][ct]);
                     }
-                // one MFMA, then two vector instructions (finer groups than
-                // three and six measured about 6% faster on varlen16)
+                if (kq + 1 < D / 32) {
+#pragma unroll
+                    for (int vt = 0; vt < NVT; ++vt) {
+                        bh[cur ^ 1][vt] = acc_frag_hi<32>(st[2 * kq + 2][vt], st[2 * kq + 3][vt]);
+                        if constexpr (NO > 0)
+                            sm.hs[wave % (NO > 0 ? NO : 1)][kq + 1][vt][lane] = __builtin_bit_cast(uint4, bh[cur ^ 1][vt]);
+                    }
+                }
 #pragma unroll
                 for (int i = 0; i < 12 * NVT; ++i) {
                     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
                     __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);   // VALU
                 }
                 __builtin_amdgcn_sched_barrier(0);
+                if (s0lo) {
+#pragma unroll
+                    for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                        for (int vt = 0; vt < NVT; ++vt) ks[ct][vt] = mma(ak[cur][ct], bl[cur][vt], ks[ct][vt]);
+                    if (kq + 1 < D / 32) {
+#pragma unroll
+                        for (int vt = 0; vt < NVT; ++vt)
+                            bl[cur ^ 1][vt] = acc_frag_lo32(st[2 * kq + 2][vt], st[2 * kq + 3][vt], bh[cur ^ 1][vt]);
+                    }
+#pragma unroll
+                    for (int i = 0; i < NCT * NVT; ++i) {
+                        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+                        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);   // VALU
+                    }
+                }
+                __builtin_amdgcn_sched_barrier(0);
             }
             if constexpr (NO > 0) signal(&sm.cnt[CNT_HAND0 + 4 * wave + 0], lane);
             // W = V - diag(exp(gamma)) K S0^T (in ks)
-            wait_seen(&sm.cnt[CNT_READY0 + xs % NP], (unsigned)(xs / NP + 1), rdy_seen, fault);
             // T operands of U = T diag(beta) W, read now so that their latency
             // hides behind the vector work of W
             bf16x8_t tah[NCT][2], tal[NCT][2];
@@ -901,6 +953,11 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
             signal(&sm.cnt[CNT_DONE], lane);
             seen_stg = peek(&sm.cnt[CNT_STG]);
             seen_rdy = peek(&sm.cnt[CNT_READY0 + (xs + 1) % NP]);
+            // read after the counter (the LDS serves a wave's operations in
+            // order; the fence keeps the compiler from swapping them), so a
+            // ready value seen means this is the published decay
+            __atomic_signal_fence(__ATOMIC_SEQ_CST);
+            seen_egl = __hip_atomic_load(&sm.slot[(xs + 1) % NP].eg[C - 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             if constexpr (NO > 0) {
                 seen_hs = peek(&sm.cnt[CNT_HAND0 + 4 * wave + 1]);
                 seen_hu = peek(&sm.cnt[CNT_HAND0 + 4 * wave + 3]);

@@ -14,6 +14,17 @@ import numpy as np
 OUT_TOL = 2e-2
 STATE_TOL = 1e-3
 
+# (test, check, what, error) of every parity check in this run, printed at the
+# end of the session by the terminal-summary hook in conftest.py.
+RESULTS = []
+
+
+def record(check, what, err):
+    import os
+
+    test = os.environ.get("PYTEST_CURRENT_TEST", "?").split(" ")[0]
+    RESULTS.append((test, check, what, err))
+
 
 def device():
     import torch
@@ -64,6 +75,7 @@ def check_outputs(got_bits, ref, what=""):
 
     err = max_abs(to_f64(got_bits), ref)
     note(f"  {what} outputs max-abs {err:.3e} (gate {OUT_TOL})")
+    record("outputs max-abs", what, err)
     assert err <= OUT_TOL, f"{what}: output max-abs {err:.3e} > {OUT_TOL}"
     return err
 
@@ -73,5 +85,6 @@ def check_states(got, ref, what=""):
     worst = float(np.max(errs)) if errs.size else 0.0
     glob = float(np.linalg.norm(np.asarray(got, np.float64) - ref) / max(np.linalg.norm(ref), 1e-300))
     note(f"  {what} states rel-Frobenius worst unit {worst:.3e}, global {glob:.3e} (gate {STATE_TOL})")
+    record("states rel-F worst unit", what, worst)
     assert worst <= STATE_TOL, f"{what}: state rel-Frobenius {worst:.3e} > {STATE_TOL}"
     return worst

@@ -3,7 +3,7 @@ import numpy as np
 import pytest
 
 import oracle.gdn_ref as ref
-from gpu_helpers import (bf16_np, check_outputs, check_states, device, note, to_dev)
+from gpu_helpers import (bf16_np, check_outputs, check_states, device, note, record, to_dev)
 from paper_2607_17979_amd import gdn
 from paper_2607_17979_amd import workloads as wl
 
@@ -104,6 +104,7 @@ def test_decode_sweep_100_steps(B, seed_off):
         worst_o = max(worst_o, float(np.max(np.abs(got - o_ref[:, 0]))))
     torch.cuda.synchronize()
     note(f"  sweep B={B}: outputs max-abs over {steps} steps {worst_o:.3e}")
+    record("outputs max-abs", f"sweep B={B}", worst_o)
     assert worst_o <= 2e-2
     got_s = state[torch.as_tensor(bs, device=dev), torch.as_tensor(hs, device=dev)].cpu().numpy()
     check_states(got_s, S[:, 0], f"sweep B={B}")

@@ -8,7 +8,7 @@ import pytest
 
 import oracle.gdn_ref as ref
 from gpu_helpers import (OUT_TOL, STATE_TOL, bf16_np, check_outputs, check_states, device, note,
-                         rel_frob_units, to_dev)
+                         rel_frob_units, to_dev, record)
 from paper_2607_17979_amd import gdn
 from paper_2607_17979_amd import workloads as wl
 
@@ -78,6 +78,8 @@ def test_long_context_three_seeds(seed):
         eo, es = _unit_check(x, o, fin, n, h, L, H_qk, H_v, f"long seed {seed}")
         worst_o, worst_s = max(worst_o, eo), max(worst_s, es)
     note(f"  long seed {seed}: worst outputs {worst_o:.3e}, worst state {worst_s:.3e}")
+    record("outputs max-abs", "", worst_o)
+    record("states rel-F worst unit", "", worst_s)
     assert worst_o <= OUT_TOL and worst_s <= STATE_TOL
 
 
@@ -111,6 +113,8 @@ def test_varlen16_every_unit():
                 worst_o = max(worst_o, float(np.max(np.abs(out - o_ref))))
                 worst_s = max(worst_s, float(rel_frob_units(fin_np[nn, h], s_ref)))
     note(f"  varlen16 all 512 units: outputs max-abs {worst_o:.3e}, worst state rel-Frobenius {worst_s:.3e}")
+    record("outputs max-abs", "", worst_o)
+    record("states rel-F worst unit", "", worst_s)
     assert worst_o <= OUT_TOL and worst_s <= STATE_TOL
 
 
@@ -155,6 +159,8 @@ def test_slow_decay_long_sequences(shape, g_scale):
         eo, es = _unit_check(x, o, fin, n, h, L, H_qk, H_v, f"slow decay {g_scale} ({label})", scale=D ** -0.5)
         worst_o, worst_s = max(worst_o, eo), max(worst_s, es)
     note(f"  slow decay {g_scale} ({label}): worst outputs {worst_o:.3e}, worst state {worst_s:.3e}")
+    record("outputs max-abs", "", worst_o)
+    record("states rel-F worst unit", "", worst_s)
     assert worst_o <= OUT_TOL and worst_s <= STATE_TOL
 
 
@@ -193,6 +199,8 @@ def test_slow_decay_token_by_token_route(g_scale):
                                  init_host=init_host[n, h], scale=D ** -0.5)
             worst_o, worst_s = max(worst_o, eo), max(worst_s, es)
     note(f"  token by token {g_scale}: worst outputs {worst_o:.3e}, worst state {worst_s:.3e}")
+    record("outputs max-abs", "", worst_o)
+    record("states rel-F worst unit", "", worst_s)
     assert worst_o <= OUT_TOL and worst_s <= STATE_TOL
 
 
@@ -239,4 +247,52 @@ def test_more_than_4096_sequences_keep_given_order():
         worst_o = max(worst_o, float(np.max(np.abs(out - o_ref))) if out.size else 0.0)
         worst_s = max(worst_s, float(rel_frob_units(fin_np[n, h], s_ref)))
     note(f"  {N} sequences: {len(units)} units, outputs max-abs {worst_o:.3e}, worst state {worst_s:.3e}")
+    record("outputs max-abs", "", worst_o)
+    record("states rel-F worst unit", "", worst_s)
+    assert worst_o <= OUT_TOL and worst_s <= STATE_TOL
+
+
+GATE_SHAPES = [(2, 2, 4, "four workgroups per head, output waves"), (5, 16, 32, "one workgroup per head")]
+
+
+@pytest.mark.parametrize("shape", GATE_SHAPES, ids=[s[3] for s in GATE_SHAPES])
+def test_decay_gate_of_the_s0_lo_product(shape):
+    """The chunk kernel drops the lo half of S0 in K S0^T in a chunk whose total
+    decay exp(gamma_last) is at most 1/16.  Chunks cycle through a total decay
+    just below that (0.9 / 16: dropped), just above it (1.1 / 16: kept),
+    fast decay (g = -softplus(x): dropped) and none (g = 0: kept), with beta in
+    [0.9, 1) and a nonzero initial state, over 40 chunks per sequence: outputs
+    and states of every unit against the oracle over all tokens."""
+    import torch
+
+    N, H_qk, H_v, label = shape
+    D, C, nch = 128, 64, 40
+    L = C * nch
+    dev = device()
+    note(f"decay gate: {N} x {L} tokens, H_v={H_v} ({label})")
+    inp = wl.prefill_inputs(960 + N, [L] * N, H_qk, H_v, D, state_std=0.02, scale=D ** -0.5)
+    rng = np.random.default_rng(961)
+    g = inp.g.reshape(N, nch, C, H_v)
+    for c in range(nch):
+        mode = c % 4
+        if mode == 0:
+            g[:, c] = np.log(0.9 / 16) / C
+        elif mode == 1:
+            g[:, c] = np.log(1.1 / 16) / C
+        elif mode == 3:
+            g[:, c] = 0.0
+    inp.g = np.ascontiguousarray(g.reshape(N * L, H_v)).astype(np.float32)
+    inp.beta = rng.uniform(0.9, 1.0, size=inp.beta.shape).astype(np.float32)
+    q, k, v = (to_dev(a, dev, bf16=True) for a in (inp.q, inp.k, inp.v))
+    g_d, b_d, cu, init = (to_dev(a, dev) for a in (inp.g, inp.beta, inp.cu_seqlens, inp.initial_state))
+    fin = torch.empty_like(init)
+    o = torch.empty((N * L, H_v, D), dtype=torch.bfloat16, device=dev)
+    ws = _workspace(N, N * L, H_v, D, dev)
+    gdn.gdn_prefill_varlen(q, k, v, g_d, b_d, cu, init, fin, o, scale=inp.scale, workspace=ws)
+    torch.cuda.synchronize()
+    assert _fault(ws, N) == 0
+    o_ref, s_ref = ref.prefill_varlen(inp.q, inp.k, inp.v, inp.g, inp.beta, inp.cu_seqlens,
+                                      inp.initial_state, scale=inp.scale)
+    worst_o = check_outputs(bf16_np(o), o_ref, f"decay gate ({label})")
+    worst_s = check_states(fin.cpu().numpy(), s_ref, f"decay gate ({label})")
     assert worst_o <= OUT_TOL and worst_s <= STATE_TOL

@@ -3,7 +3,7 @@ import numpy as np
 import pytest
 
 import oracle.gdn_ref as ref
-from gpu_helpers import (bf16_np, check_outputs, check_states, device, note, rel_frob_units, to_dev)
+from gpu_helpers import (bf16_np, check_outputs, check_states, device, note, record, rel_frob_units, to_dev)
 from paper_2607_17979_amd import gdn
 from paper_2607_17979_amd import workloads as wl
 
@@ -98,6 +98,8 @@ def _sampled_check(inp, o, fin, units, what):
         worst_s = max(worst_s, float(rel_frob_units(fin_np[n, h], s_ref)))
     note(f"  {what}: {len(units)} units, outputs max-abs {worst_o:.3e}, "
          f"states worst rel-Frobenius {worst_s:.3e}")
+    record("outputs max-abs", what, worst_o)
+    record("states rel-F worst unit", what, worst_s)
     assert worst_o <= 2e-2
     assert worst_s <= 1e-3
 
