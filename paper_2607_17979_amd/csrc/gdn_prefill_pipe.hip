@@ -60,7 +60,7 @@ constexpr int SBS = 16 * SP + 4;
 constexpr int kSpinLimit = 1 << 20;
 // K S0^T takes the lo half of S0 only when the chunk's total decay
 // exp(gamma_last) exceeds this (see the state waves' first phase).
-constexpr float kS0LoDecay = 1.f / 16;
+constexpr float kS0LoDecay = 1.f / 256;
 
 __device__ __forceinline__ constexpr int bidx(int i, int j) { return i * (i + 1) / 2 + j; }
 

@@ -258,8 +258,8 @@ GATE_SHAPES = [(2, 2, 4, "four workgroups per head, output waves"), (5, 16, 32, 
 @pytest.mark.parametrize("shape", GATE_SHAPES, ids=[s[3] for s in GATE_SHAPES])
 def test_decay_gate_of_the_s0_lo_product(shape):
     """The chunk kernel drops the lo half of S0 in K S0^T in a chunk whose total
-    decay exp(gamma_last) is at most 1/16.  Chunks cycle through a total decay
-    just below that (0.9 / 16: dropped), just above it (1.1 / 16: kept),
+    decay exp(gamma_last) is at most 1/256.  Chunks cycle through a total
+    decay just below that (0.9 / 256: dropped), just above it (1.1 / 256: kept),
     fast decay (g = -softplus(x): dropped) and none (g = 0: kept), with beta in
     [0.9, 1) and a nonzero initial state, over 40 chunks per sequence: outputs
     and states of every unit against the oracle over all tokens."""
@@ -276,9 +276,9 @@ def test_decay_gate_of_the_s0_lo_product(shape):
     for c in range(nch):
         mode = c % 4
         if mode == 0:
-            g[:, c] = np.log(0.9 / 16) / C
+            g[:, c] = np.log(0.9 / 256) / C
         elif mode == 1:
-            g[:, c] = np.log(1.1 / 16) / C
+            g[:, c] = np.log(1.1 / 256) / C
         elif mode == 3:
             g[:, c] = 0.0
     inp.g = np.ascontiguousarray(g.reshape(N * L, H_v)).astype(np.float32)
