@@ -154,10 +154,14 @@ GDN_API size_t gdn_prefill_workspace_size(int N, int T, int H_v, int D_k, int D_
  *   cu_seqlens     int32 [N + 1], device: sequence n is tokens
  *                  [cu_seqlens[n], cu_seqlens[n+1]).  Must hold cu[0] = 0,
  *                  non-decreasing, cu[N] = T.  The library never reads it on
- *                  the host and trusts it: a violation is undefined behaviour
- *                  (out-of-bounds device reads included).  Zero-length
- *                  sequences are allowed: their final state is their initial
- *                  state.
+ *                  the host; on the device every kernel clamps each
+ *                  sequence's offsets into [0, T] (begin clamp(cu[n], 0, T),
+ *                  end clamp(cu[n+1], begin, T)), so a malformed cu_seqlens
+ *                  never leads to an access outside the T tokens, and the
+ *                  call's first launch checks it and sets bit 2 of the fault
+ *                  word (see workspace): the results of such a call are
+ *                  meaningless.  Zero-length sequences are allowed: their
+ *                  final state is their initial state.
  *   initial_state  fp32 [N, H_v, D, D] or NULL (zero state)
  *   final_state    fp32 [N, H_v, D, D]; may be the same pointer as
  *                  initial_state (in-place), must not partially overlap it.
@@ -166,10 +170,11 @@ GDN_API size_t gdn_prefill_workspace_size(int N, int T, int H_v, int D_k, int D_
  *                  gdn_prefill_workspace_size(...) bytes, 256-byte aligned;
  *                  its contents are scratch (overwritten by each call).  Once
  *                  the call has completed on the stream, int32 word N + 1 of
- *                  it is 0, or has bit 0 set if a wave of the chunk kernel
- *                  gave up one of its bounded waits for another wave (a
- *                  broken synchronisation, never expected): the call's
- *                  results are then invalid.  A diagnostic read, not a status
+ *                  it (the fault word) is 0, or has bit 0 set if a wave of
+ *                  the chunk kernel gave up one of its bounded waits for
+ *                  another wave (a broken synchronisation, never expected),
+ *                  or bit 2 if cu_seqlens was malformed: the call's results
+ *                  are then invalid.  A diagnostic read, not a status
  *                  the call returns (the call does not wait for its kernels);
  *                  a call that is a no-op (N = 0) leaves the workspace as it
  *                  was.

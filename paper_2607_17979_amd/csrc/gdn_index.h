@@ -28,6 +28,26 @@ __host__ __device__ inline int logical_item(int bid, int total) {
     return grp * G + P * (r & 7) + (r >> 3);
 }
 
+// Tokens [beg, beg + len) of sequence n, its offsets clamped into [0, T]: beg =
+// clamp(cu[n], 0, T), end = clamp(cu[n + 1], beg, T).  For a valid cu_seqlens
+// (cu[0] = 0, non-decreasing, cu[N] = T) this is cu[n] and cu[n + 1] - cu[n];
+// for any other it still names no token outside [0, T), so a malformed
+// cu_seqlens gives meaningless results but no access outside the buffers.
+struct SeqSpan {
+    int beg, len;
+};
+__host__ __device__ inline SeqSpan seq_span(const int32_t* cu, int n, int T) {
+    int a = cu[n], b = cu[n + 1];
+    a = a < 0 ? 0 : (a > T ? T : a);
+    b = b < a ? a : (b > T ? T : b);
+    return SeqSpan{a, b - a};
+}
+// Whether entry i of cu_seqlens breaks validity: cu[0] != 0, cu[N] != T, or
+// cu[i + 1] < cu[i] (i in [0, N)); cu_seqlens is valid iff no i breaks it.
+__host__ __device__ inline bool cu_seqlens_breaks(const int32_t* cu, int N, int T, int i) {
+    return cu[i + 1] < cu[i] || (i == 0 && cu[0] != 0) || (i == N - 1 && cu[N] != T);
+}
+
 // Rank of sequence i when sequences are ordered by decreasing length, ties by
 // index (len: the N lengths).
 __host__ __device__ inline int longest_first_rank(const int* len, int N, int i) {
@@ -46,10 +66,10 @@ __host__ __device__ inline int longest_first_rank(const int* len, int N, int i) 
 
 // Whether unit u runs in the token-by-token kernel: its sequence has at most
 // recur_max tokens and its state lies inside the pool (with state_idx).
-__host__ __device__ inline bool recur_unit_runs(long u, int bph, int H_v, const int32_t* cu,
+__host__ __device__ inline bool recur_unit_runs(long u, int bph, int H_v, const int32_t* cu, int T,
                                                 const int32_t* state_idx, int P, int recur_max) {
     const int n = (int)(u / bph / H_v);
-    if (cu[n + 1] - cu[n] > recur_max) return false;
+    if (seq_span(cu, n, T).len > recur_max) return false;
     if (state_idx != nullptr) {
         const int slot = state_idx[n];
         if (slot < 0 || slot >= P) return false;
@@ -74,9 +94,9 @@ __host__ __device__ inline long recur_slot_unit(long s, long units, int grp) {
 // The first slot at or after s (stepping by stride) whose unit runs here, or
 // a value >= units.
 __host__ __device__ inline long recur_next_slot(long s, long stride, long units, int grp, int bph, int H_v,
-                                                const int32_t* cu, const int32_t* state_idx, int P,
+                                                const int32_t* cu, int T, const int32_t* state_idx, int P,
                                                 int recur_max) {
-    while (s < units && !recur_unit_runs(recur_slot_unit(s, units, grp), bph, H_v, cu, state_idx, P, recur_max))
+    while (s < units && !recur_unit_runs(recur_slot_unit(s, units, grp), bph, H_v, cu, T, state_idx, P, recur_max))
         s += stride;
     return s;
 }
@@ -87,7 +107,7 @@ struct RecurUnit {
     long u, shead;
     int h, hq, blk, t0, len;
 };
-__host__ __device__ inline RecurUnit recur_unit_at(long u, int bph, int H_v, int H_qk, const int32_t* cu,
+__host__ __device__ inline RecurUnit recur_unit_at(long u, int bph, int H_v, int H_qk, const int32_t* cu, int T,
                                                    const int32_t* state_idx) {
     RecurUnit r;
     const long head = u / bph;  // n H_v + h
@@ -96,8 +116,9 @@ __host__ __device__ inline RecurUnit recur_unit_at(long u, int bph, int H_v, int
     r.h = (int)(head - (long)n * H_v);
     r.hq = r.h / (H_v / H_qk);
     r.blk = (int)(u - head * bph);
-    r.t0 = cu[n];
-    r.len = cu[n + 1] - r.t0;
+    const SeqSpan sp = seq_span(cu, n, T);
+    r.t0 = sp.beg;
+    r.len = sp.len;
     r.shead = state_idx != nullptr ? (long)state_idx[n] * H_v + r.h : head;
     return r;
 }
@@ -120,7 +141,7 @@ struct PipeItem {
     long slot;
 };
 __host__ __device__ inline PipeItem pipe_item_fields(int item, int vsplit, int H_v, int H_qk,
-                                                     const int32_t* order, const int32_t* cu,
+                                                     const int32_t* order, const int32_t* cu, int T,
                                                      const int32_t* state_idx, int P, int chunk,
                                                      int recur_max) {
     PipeItem it;
@@ -130,8 +151,9 @@ __host__ __device__ inline PipeItem pipe_item_fields(int item, int vsplit, int H
     it.h = head_item - rank * H_v;
     it.n = order[rank];
     it.hq = it.h / (H_v / H_qk);
-    it.seq_beg = cu[it.n];
-    it.seq_len = cu[it.n + 1] - it.seq_beg;
+    const SeqSpan sp = seq_span(cu, it.n, T);
+    it.seq_beg = sp.beg;
+    it.seq_len = sp.len;
     it.nch = it.seq_len <= recur_max ? 0 : (it.seq_len + chunk - 1) / chunk;
     it.slot = it.n;
     if (state_idx != nullptr) {

@@ -63,9 +63,10 @@ int device_compute_units();
 // Workspace layout of the prefill: int32 order[N] (sequence indices sorted by
 // length, longest first, ties by index), then (d = 128) int32 order[N] = the
 // number of sequences longer than kRecurMax, then int32 order[N + 1] = the
-// fault word (cleared by the call's first launch; bit 0 set by any wave of the
+// fault word (written by the call's first launch; bit 0 set by any wave of the
 // chunk kernel whose counter wait ran out of its bound, bit 1 by a short-only
-// call that met a longer sequence); rounded up to 256 bytes.
+// call that met a longer sequence, bit 2 by a malformed cu_seqlens); rounded up
+// to 256 bytes.
 size_t prefill_workspace_bytes(int N);
 
 }  // namespace gdn

@@ -85,10 +85,13 @@ struct Smem {
 
 // --- schedule: sequences by length, longest first (ties by index) ---------------
 __global__ __launch_bounds__(256) void prefill_schedule_kernel(const int32_t* __restrict__ cu,
-                                                               int N, int32_t* __restrict__ order) {
+                                                               int N, int T, int32_t* __restrict__ order) {
     __shared__ int len[kSortMax];
-    if (threadIdx.x == 0) order[N + 1] = 0;  // no waits here: the fault word stays clear
-    schedule_longest_first(cu, N, order, len);
+    __shared__ int cnt[2];
+    bool bad = false;
+    schedule_longest_first(cu, N, T, order, len, cnt, 0, &bad);
+    // the fault word: no waits here, so only bit 2 (a malformed cu_seqlens)
+    if (threadIdx.x == 0) order[N + 1] = bad ? 4 : 0;
 }
 
 // --- the chunk kernel ----------------------------------------------------------
@@ -98,7 +101,7 @@ __global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
     const uint16_t* __restrict__ v, const float* __restrict__ g,
     const float* __restrict__ beta, const int32_t* __restrict__ cu,
     const int32_t* __restrict__ order, const float* initial_state, float* final_state,
-    uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale,
+    uint16_t* __restrict__ o, int N, int T, int H_qk, int H_v, float scale,
     const int32_t* __restrict__ state_idx, int P_slots, int flags) {
     typedef Cfg<D, C> P;
     constexpr int KD = P::KD, KC = P::KC;
@@ -117,8 +120,9 @@ __global__ __launch_bounds__((Cfg<D, C>::NT)) void prefill_kernel(
     const int h = item - rank * H_v;
     const int n = order[rank];
     const int hq = h / (H_v / H_qk);
-    const int seq_beg = cu[n];
-    const int seq_len = cu[n + 1] - seq_beg;
+    const SeqSpan sp = seq_span(cu, n, T);
+    const int seq_beg = sp.beg;
+    const int seq_len = sp.len;
     const int vcol0 = wave * P::VW;
     // the state of sequence n: state n, or pool slot state_idx[n] (outside the
     // pool: the sequence is skipped)
@@ -498,14 +502,14 @@ hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {
         if (e != hipSuccess || a.T <= kRecurMax || a.short_only) return e;
         return launch_prefill_pipe(a, order, stream);
     }
-    hipLaunchKernelGGL(prefill_schedule_kernel, dim3(1), dim3(256), 0, stream, a.cu_seqlens, a.N, order);
+    hipLaunchKernelGGL(prefill_schedule_kernel, dim3(1), dim3(256), 0, stream, a.cu_seqlens, a.N, a.T, order);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     typedef Cfg<16, 16> P16;
     hipLaunchKernelGGL((prefill_kernel<16, 16>), dim3((unsigned)(a.N * a.H_v)), dim3(P16::NT), 0,
                        stream, (const uint16_t*)a.q, (const uint16_t*)a.k, (const uint16_t*)a.v, a.g,
                        a.beta, a.cu_seqlens, (const int32_t*)order, a.initial_state, a.final_state,
-                       (uint16_t*)a.o, a.N, a.H_qk, a.H_v, a.scale, a.state_idx, a.P, a.flags);
+                       (uint16_t*)a.o, a.N, a.T, a.H_qk, a.H_v, a.scale, a.state_idx, a.P, a.flags);
     return hipGetLastError();
 }
 

@@ -587,7 +587,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const float* __restrict__ g, const float* __restrict__ beta, const int32_t* __restrict__ cu,
     const int32_t* __restrict__ order, const float* initial_state, float* final_state,
-    uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale,
+    uint16_t* __restrict__ o, int N, int T, int H_qk, int H_v, float scale,
     const int32_t* __restrict__ state_idx, int P, int* fault) {
     constexpr bool NORM = (PRO & kFlagQkL2Norm) != 0;
     constexpr int VW = 16 * NVT;        // value columns per state wave
@@ -615,7 +615,7 @@ __global__ __launch_bounds__(64 * (NS + NO + NP)) void prefill_pipe_kernel(
     auto item_at = [&](int pass) -> int { return pipe_item_at<VSPLIT>(pass, G, bid, items); };
     typedef PipeItem Item;
     auto decode = [&](int item) -> Item {
-        return pipe_item_fields(item, VSPLIT, H_v, H_qk, order, cu, state_idx, P, C, kRecurMax);
+        return pipe_item_fields(item, VSPLIT, H_v, H_qk, order, cu, T, state_idx, P, C, kRecurMax);
     };
     const size_t qk_stride = (size_t)H_qk * D;
     const size_t v_stride = (size_t)H_v * D;
@@ -1149,7 +1149,7 @@ static hipError_t launch_pipe_pro(const PrefillArgs& a, int32_t* order, hipStrea
     hipLaunchKernelGGL((pipe::prefill_pipe_kernel<NS, NVT, NO, PRO>), dim3((unsigned)grid),
                        dim3(64 * (NS + NO + pipe::NP)), 0, stream, (const uint16_t*)a.q, (const uint16_t*)a.k,
                        (const uint16_t*)a.v, a.g, a.beta, a.cu_seqlens, order, a.initial_state, a.final_state,
-                       (uint16_t*)a.o, a.N, a.H_qk, a.H_v, a.scale, a.state_idx, a.P, order + a.N + 1);
+                       (uint16_t*)a.o, a.N, a.T, a.H_qk, a.H_v, a.scale, a.state_idx, a.P, order + a.N + 1);
     return hipGetLastError();
 }
 

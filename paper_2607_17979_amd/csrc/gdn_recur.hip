@@ -60,25 +60,23 @@ __global__ __launch_bounds__(256) void prefill_recur_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const float* __restrict__ g, const float* __restrict__ beta, const int32_t* __restrict__ cu,
     int32_t* __restrict__ order, const float* initial_state, float* final_state,
-    uint16_t* __restrict__ o, int N, int H_qk, int H_v, float scale,
+    uint16_t* __restrict__ o, int N, int T, int H_qk, int H_v, float scale,
     const int32_t* __restrict__ state_idx, int P, int short_only, int flags) {
     __shared__ Smem sm;
-    __shared__ int nlong;
+    __shared__ int cnt[2];
     if (blockIdx.x == 0) {
         // the chunk kernel's schedule (not needed when no chunk kernel
-        // follows), then the number of sequences it runs
-        if (!short_only) schedule_longest_first(cu, N, order, sm.sched_len);
-        if (threadIdx.x == 0) nlong = 0;
-        __syncthreads();
-        int mine = 0;
-        for (int i = threadIdx.x; i < N; i += blockDim.x) mine += cu[i + 1] - cu[i] > kRecurMax;
-        if (mine) atomicAdd(&nlong, mine);
-        __syncthreads();
+        // follows), the number of sequences it runs and the check of
+        // cu_seqlens, from one read of it
+        bool bad = false;
+        const int nlong =
+            schedule_longest_first(cu, N, T, short_only ? nullptr : order, sm.sched_len, cnt, kRecurMax, &bad);
         if (threadIdx.x == 0) {
             order[N] = nlong;
             // the fault word: a short-only call that met a longer sequence
-            // (skipped) sets bit 1; the chunk kernel may set bit 0 later
-            order[N + 1] = (short_only && nlong > 0) ? 2 : 0;
+            // (skipped) sets bit 1, a malformed cu_seqlens bit 2; the chunk
+            // kernel may set bit 0 later
+            order[N + 1] = ((short_only && nlong > 0) ? 2 : 0) | (bad ? 4 : 0);
         }
         return;
     }
@@ -95,13 +93,13 @@ __global__ __launch_bounds__(256) void prefill_recur_kernel(
     const long stride = gridDim.x - 1;
     const int grp = (H_v / H_qk) * BPH;
     auto next_unit = [&](long s) -> long {
-        return recur_next_slot(s, stride, units, grp, BPH, H_v, cu, state_idx, P, kRecurMax);
+        return recur_next_slot(s, stride, units, grp, BPH, H_v, cu, T, state_idx, P, kRecurMax);
     };
     // The fields of the unit in slot s: its state (state n, or pool slot
     // state_idx[n]), head, row block and tokens.
     typedef RecurUnit Unit;
     auto unit_at = [&](long s) -> Unit {
-        return recur_unit_at(recur_slot_unit(s, units, grp), BPH, H_v, H_qk, cu, state_idx);
+        return recur_unit_at(recur_slot_unit(s, units, grp), BPH, H_v, H_qk, cu, T, state_idx);
     };
     auto state_row = [&](const Unit& x) {
         const int row = x.blk * ROWS + wave * ROWS_PER_WAVE + sub;
@@ -226,7 +224,7 @@ hipError_t launch_prefill_recur(const PrefillArgs& a, int32_t* order, hipStream_
     const long grid = 1 + std::max<long>(1, std::min<long>(units, 8L * device_compute_units()));
     hipLaunchKernelGGL(recur::prefill_recur_kernel, dim3((unsigned)grid), dim3(64 * recur::NWAVE), 0, stream,
                        (const uint16_t*)a.q, (const uint16_t*)a.k, (const uint16_t*)a.v, a.g, a.beta,
-                       a.cu_seqlens, order, a.initial_state, a.final_state, (uint16_t*)a.o, a.N, a.H_qk,
+                       a.cu_seqlens, order, a.initial_state, a.final_state, (uint16_t*)a.o, a.N, a.T, a.H_qk,
                        a.H_v, a.scale, a.state_idx, a.P, a.short_only ? 1 : 0, a.flags);
     return hipGetLastError();
 }

@@ -156,7 +156,9 @@ def workspace_fault(workspace, N: int) -> int:
     """The wait-fault word of a prefill workspace after the call that used it
     has completed (synchronises the device): 0, or bit 0 set if a wave of the
     chunk kernel gave up a bounded wait (results invalid), bit 1 set if
-    gdn_decode_multitoken met a sequence longer than 8 tokens."""
+    gdn_decode_multitoken met a sequence longer than 8 tokens, bit 2 set if
+    cu_seqlens was malformed (results meaningless; no access went outside the
+    T tokens)."""
     import torch
 
     torch.cuda.synchronize(workspace.device)

@@ -222,3 +222,34 @@ def test_work_walks_under_sanitizers(bins, seed):
             by_total.setdefault(total, []).append(item)
         for total, its in by_total.items():
             assert sorted(its) == list(range(total)), (key, total)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_malformed_cu_seqlens_stays_in_bounds(bins, seed):
+    """Every kernel takes a sequence's tokens from seq_span: for any cu_seqlens,
+    valid or not, the span lies inside [0, T), and for a valid one it is the
+    plain difference; cu_seqlens_breaks flags exactly the malformed arrays (the
+    kernels set bit 2 of the fault word from it).  Host build only: no GPU run
+    is ever given a malformed cu_seqlens."""
+    rng = np.random.default_rng(2000 + seed)
+    for trial in range(40):
+        N = int(rng.integers(1, 30))
+        T = int(rng.integers(0, 500))
+        if trial % 4 == 0:  # valid
+            cut = np.sort(rng.integers(0, T + 1, size=N - 1)) if N > 1 else np.zeros(0, np.int64)
+            cu = np.concatenate([[0], cut, [T]]).astype(np.int64)
+        else:  # arbitrary, including negative, decreasing and past-the-end offsets
+            cu = rng.integers(-50, T + 100, size=N + 1)
+            if trial % 4 == 1:
+                cu = np.sort(cu)
+        text = "spans\n%d %d\n%s\n" % (N, T, " ".join(map(str, cu)))
+        rows = {}
+        for ln in _run(bins["walk"], text).splitlines():
+            f = ln.split()
+            rows.setdefault(f[0], []).append(tuple(int(x) for x in f[1:]))
+        valid = cu[0] == 0 and cu[N] == T and bool(np.all(np.diff(cu) >= 0))
+        assert (not any(b for _, b in rows["breaks"])) == valid
+        for n, beg, ln in rows["span"]:
+            assert 0 <= beg <= T and 0 <= ln and beg + ln <= T
+            if valid:
+                assert (beg, ln) == (int(cu[n]), int(cu[n + 1] - cu[n]))
