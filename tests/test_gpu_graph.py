@@ -7,7 +7,8 @@ states by one call; after each of three replays, with eager calls of the same
 step and synchronisations in between, the graph's states and outputs must
 equal the eager ones bit for bit.  The batches mix sequences of at most 8
 tokens (token-by-token launch), longer ones (chunk kernel) and an empty one;
-both head dims."""
+both head dims.  Also: calls issued on a side stream (the binding's stream
+argument) match those on the current stream bit for bit."""
 import pytest
 
 from gpu_helpers import device, note, to_dev
@@ -65,3 +66,47 @@ def test_prefill_graph_replay_matches_eager(D, entry):
         if entry == "workspace":
             assert gdn.workspace_fault(ws, N) == 0
     assert not torch.equal(s_graph, state0), "the replays must advance the states"
+
+
+def test_calls_on_a_side_stream_match_the_current_stream():
+    """The binding's stream argument: a decode step and a prefill call (with
+    the workspace the binding allocates on the launch stream) issued on a side
+    stream while the current stream is kept busy give bit for bit the results
+    of the same calls on the current stream."""
+    import torch
+
+    dev = device()
+    note("decode and prefill on a side stream")
+    d = wl.decode_inputs(911, 16, 16, 32, 128)
+    dq, dk, dv = (to_dev(a, dev, bf16=True) for a in (d.q, d.k, d.v))
+    dg, db = to_dev(d.g, dev), to_dev(d.beta, dev)
+    p = wl.prefill_inputs(912, [150, 3, 0, 64, 9], 2, 4, 128, state_std=0.02)
+    N, T, _, H_v, D = p.shape
+    pq, pk, pv = (to_dev(a, dev, bf16=True) for a in (p.q, p.k, p.v))
+    pg, pb, cu = to_dev(p.g, dev), to_dev(p.beta, dev), to_dev(p.cu_seqlens, dev)
+    init = to_dev(p.initial_state, dev)
+
+    def buffers():
+        return (to_dev(d.state, dev), torch.empty((16, 32, 128), dtype=torch.bfloat16, device=dev),
+                torch.empty((N, H_v, D, D), dtype=torch.float32, device=dev),
+                torch.empty((T, H_v, D), dtype=torch.bfloat16, device=dev))
+
+    def run(bufs, stream):
+        st, od, fin, op = bufs
+        gdn.gdn_decode(dq, dk, dv, dg, db, st, od, stream=stream)
+        ws = gdn.gdn_prefill_varlen(pq, pk, pv, pg, pb, cu, init, fin, op, stream=stream)
+        return (st, od, fin, op, ws)
+
+    ref = run(buffers(), None)
+    side_bufs = buffers()
+    busy = torch.randn((4096, 4096), device=dev)
+    torch.cuda.synchronize()
+    for _ in range(8):
+        busy = torch.mm(busy, busy) * 1e-3    # keeps the current stream busy meanwhile
+    side = torch.cuda.Stream()
+    got = run(side_bufs, side)
+    torch.cuda.synchronize()
+    assert gdn.workspace_fault(got[4], N) == 0
+    for a, b in zip(ref[:4], got[:4]):
+        assert torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a.view(torch.int32),
+                           b.view(torch.int16) if b.dtype == torch.bfloat16 else b.view(torch.int32))
