@@ -323,6 +323,11 @@ GDN_API int gdn_decode_ex(const void* q, const void* k, const void* v,
  *              gdn_decode_multitoken route: D = 128, T <= 8 N, the state
  *              updated in place, so initial_state must be NULL or equal
  *              final_state).  0 gives the plain entry points bit for bit.
+ *              GDN_SHORT_ONLY with state_idx is a multi-token decode step on
+ *              pooled states in one launch: sequence n (at most 8 tokens)
+ *              advances slot state_idx[n]; results equal
+ *              gdn_prefill_varlen_indexed bit for bit; a longer sequence is
+ *              skipped and sets bit 1 of the fault word.
  *   workspace  gdn_prefill_workspace_size(N, T, H_v, D, D, chunk) bytes, as
  *              gdn_prefill_varlen (same fault word).
  *

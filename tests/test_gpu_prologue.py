@@ -182,3 +182,66 @@ def test_multitoken_and_pool_with_prologue():
     keep = np.concatenate([np.arange(cu[n], cu[n + 1]) for n in range(len(idx)) if ok[n]])
     check_outputs(bf16_np(o2)[keep], o_ref2[keep], "pool prologue")
     check_states(pool_out.cpu().numpy()[idx[ok]], s_ref2[ok], "pool prologue")
+
+
+def test_multitoken_on_a_pool():
+    """A multi-token decode step on pooled states in one call:
+    gdn_prefill_varlen_ex with GDN_SHORT_ONLY and state_idx (the token-by-token
+    launch alone).  Slots and outputs equal gdn_prefill_varlen_indexed on the
+    same pool bit for bit (for at most 8 tokens both take the token-by-token
+    route) and match the oracle; slots not named and the output rows of
+    skipped entries (-1, past the pool) stay untouched.  A second call with a
+    9-token sequence skips it, leaves its slot and rows untouched and sets
+    bit 1 of the fault word."""
+    import torch
+
+    dev = device()
+    P, H_qk, H_v, D = 12, 16, 32, 128
+    lengths = [4, 0, 8, 2, 7, 3]
+    idx = np.array([5, 0, -1, 2, 11, 13], np.int32)
+    note(f"multi-token decode on a pool: lengths {lengths}, slots {idx.tolist()} of {P}")
+    inp = wl.prefill_inputs(85, lengths, H_qk, H_v, D, scale=D ** -0.5)
+    pool = (0.02 * np.random.default_rng(86).standard_normal((P, H_v, D, D))).astype(np.float32)
+    q, k, v = (to_dev(x, dev, bf16=True) for x in (inp.q, inp.k, inp.v))
+    g, b, cu = to_dev(inp.g, dev), to_dev(inp.beta, dev), to_dev(inp.cu_seqlens, dev)
+    sidx = to_dev(idx, dev)
+    T = int(inp.cu_seqlens[-1])
+
+    def out():
+        return torch.full((T, H_v, D), float("nan"), dtype=torch.bfloat16, device=dev)
+
+    pool_a, o_a = to_dev(pool, dev), out()
+    ws = gdn.gdn_prefill_varlen_ex(q, k, v, g, b, cu, None, pool_a, o_a, state_idx=sidx, flags=SHORT,
+                                   scale=inp.scale)
+    assert gdn.workspace_fault(ws, len(lengths)) == 0
+    pool_b, o_b = to_dev(pool, dev), out()
+    ws = gdn.gdn_prefill_varlen_indexed(q, k, v, g, b, cu, pool_b, sidx, o_b, scale=inp.scale)
+    assert gdn.workspace_fault(ws, len(lengths)) == 0
+    torch.cuda.synchronize()
+    assert torch.equal(pool_a.view(torch.int32), pool_b.view(torch.int32))
+    assert torch.equal(o_a.view(torch.int16), o_b.view(torch.int16))
+    ok = (idx >= 0) & (idx < P)
+    untouched = sorted(set(range(P)) - set(idx[ok].tolist()))
+    assert np.array_equal(pool_a.cpu().numpy()[untouched], pool[untouched])
+    cu_h = inp.cu_seqlens
+    skipped = np.concatenate([np.arange(cu_h[n], cu_h[n + 1]) for n in range(len(idx)) if not ok[n]])
+    assert bool(torch.isnan(o_a.float()[skipped]).all())
+    init = np.stack([pool[s] if ok[n] else np.zeros_like(pool[0]) for n, s in enumerate(idx)])
+    o_ref, s_ref = ref.prefill_varlen(inp.q, inp.k, inp.v, inp.g, inp.beta, inp.cu_seqlens, init,
+                                      scale=inp.scale)
+    keep = np.concatenate([np.arange(cu_h[n], cu_h[n + 1]) for n in range(len(idx)) if ok[n]])
+    check_outputs(bf16_np(o_a)[keep], o_ref[keep], "multi-token pool")
+    check_states(pool_a.cpu().numpy()[idx[ok]], s_ref[ok], "multi-token pool")
+    # a sequence longer than 8 tokens is skipped and flagged
+    inp9 = wl.prefill_inputs(87, [3, 9, 1], H_qk, H_v, D, scale=D ** -0.5)
+    idx9 = to_dev(np.array([1, 4, 7], np.int32), dev)
+    q9, k9, v9 = (to_dev(x, dev, bf16=True) for x in (inp9.q, inp9.k, inp9.v))
+    g9, b9, cu9 = to_dev(inp9.g, dev), to_dev(inp9.beta, dev), to_dev(inp9.cu_seqlens, dev)
+    pool_c = to_dev(pool, dev)
+    o_c = torch.full((13, H_v, D), float("nan"), dtype=torch.bfloat16, device=dev)
+    ws = gdn.gdn_prefill_varlen_ex(q9, k9, v9, g9, b9, cu9, None, pool_c, o_c, state_idx=idx9, flags=SHORT,
+                                   scale=inp9.scale)
+    assert gdn.workspace_fault(ws, 3) == 2
+    pc = pool_c.cpu().numpy()
+    assert np.array_equal(pc[4], pool[4]) and not np.array_equal(pc[1], pool[1])
+    assert bool(torch.isnan(o_c.float()[3:12]).all()) and not bool(torch.isnan(o_c.float()[:3]).any())
