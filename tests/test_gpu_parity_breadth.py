@@ -1,7 +1,8 @@
 """Parity breadth on the GPU: the long-context workload on three seeds, the
 full oracle over every (sequence, head) unit of the varlen workload, the
 slow-decay / high-beta regime over long sequences through every launch shape
-of the chunk kernel and through the token-by-token route, and a batch of
+of the chunk kernel (and with no decay at all over 2 x 65,536 tokens) and
+through the token-by-token route, and a batch of
 more than 4,096 sequences (the schedule then keeps the given order)."""
 import numpy as np
 import pytest
@@ -159,6 +160,35 @@ def test_slow_decay_long_sequences(shape, g_scale):
         eo, es = _unit_check(x, o, fin, n, h, L, H_qk, H_v, f"slow decay {g_scale} ({label})", scale=D ** -0.5)
         worst_o, worst_s = max(worst_o, eo), max(worst_s, es)
     note(f"  slow decay {g_scale} ({label}): worst outputs {worst_o:.3e}, worst state {worst_s:.3e}")
+    record("outputs max-abs", "", worst_o)
+    record("states rel-F worst unit", "", worst_s)
+    assert worst_o <= OUT_TOL and worst_s <= STATE_TOL
+
+
+def test_no_decay_long_context():
+    """g = 0 exactly, beta in [0.9, 1), 2 x 65,536 tokens from a nonzero
+    initial state (the long-context shape: four workgroups per head with
+    output waves): the state never forgets, so every chunk keeps the S0 lo
+    product and rounding could only accumulate over the 1,024 chunks.  The
+    oracle follows two units over all 65,536 tokens."""
+    import torch
+
+    N, H_v, L = 2, 32, 65536
+    H_qk, D = H_v // 2, 128
+    dev = device()
+    note(f"no decay, long context: {N} x {L} tokens, H_v={H_v}")
+    x = wl.prefill_inputs_device(931, N, L, H_qk, H_v, D, 0.02, dev, g_scale=0.0, beta_range=(0.9, 1.0))
+    fin = torch.empty_like(x["init"])
+    o = torch.empty((N * L, H_v, D), dtype=torch.bfloat16, device=dev)
+    ws = _workspace(N, N * L, H_v, D, dev)
+    gdn.gdn_prefill_varlen(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], x["init"], fin, o,
+                           scale=D ** -0.5, workspace=ws)
+    assert _fault(ws, N) == 0
+    worst_o = worst_s = 0.0
+    for n, h in ((0, 3), (1, H_v - 1)):
+        eo, es = _unit_check(x, o, fin, n, h, L, H_qk, H_v, "no decay, long context", scale=D ** -0.5)
+        worst_o, worst_s = max(worst_o, eo), max(worst_s, es)
+    note(f"  no decay, long context: worst outputs {worst_o:.3e}, worst state {worst_s:.3e}")
     record("outputs max-abs", "", worst_o)
     record("states rel-F worst unit", "", worst_s)
     assert worst_o <= OUT_TOL and worst_s <= STATE_TOL
