@@ -17,7 +17,8 @@
 //     registers), writes them to its result slot once the state waves are done
 //     with the slot's previous chunk, and finally stages the chunk's K, Q, V
 //     rows into LDS (K double-buffered by chunk parity, Q and V single) once
-//     the state waves have released the buffers.  A producer therefore has
+//     the state waves have released the buffers: K from the operand registers
+//     it still holds, Q and V read from memory.  A producer therefore has
 //     about four state iterations to prepare a chunk, and none of its latency
 //     is on the state waves' path.
 //
@@ -335,8 +336,8 @@ __device__ __forceinline__ uint4 ld16(const void* base, unsigned byte_off) {
     return *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(base) + byte_off);
 }
 // Streaming load of the V rows (read once), marked non-temporal so that it
-// does not push out of L2 the K and Q rows that the producers read twice
-// (operand fragments, then staging a few chunks later).
+// does not push out of L2 the Q rows that the producers read twice (operand
+// fragments, then staging a few chunks later).
 typedef unsigned u32x4v_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint4 ld16_stream(const void* base, unsigned byte_off) {
     const u32x4v_t r =
@@ -531,28 +532,29 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
     sl.egl[lane] = fast_exp(glast - gx);
     signal(&sm.cnt[CNT_READY0 + pc.pw], lane);
     // ---- stage the chunk's K, Q, V rows once the state waves have
-    //      released the previous chunk's (row 4 it + gq, segment m);
+    //      released the previous chunk's (Q: row 4 it + gq, segment m);
     //      stream chunk 0 was staged by the whole workgroup
     if (x == 0) return;
     // (The zero stores before the loads are dead; without them the compiler
     // kept these arrays in scratch memory across the waits below.)
-    uint4 sk[SITEMS], sq[SITEMS];
+    uint4 sq[SITEMS];
 #pragma unroll
     for (int it = 0; it < SITEMS; ++it) {
         const unsigned off = (unsigned)min(4 * it + gq, L - 1) * qks + 8u * m;
-        sk[it] = sq[it] = uint4{0, 0, 0, 0};
-        sk[it] = ld16(kc0, 2u * off);
+        sq[it] = uint4{0, 0, 0, 0};
         sq[it] = ld16(qc0, 2u * off);
-        if constexpr (NORM) {
-            const int row = min(4 * it + gq, L - 1);
-            sk[it] = scale_bf16x8(sk[it], rnk[row]);
-            sq[it] = scale_bf16x8(sq[it], rnq[row]);
-        }
+        if constexpr (NORM) sq[it] = scale_bf16x8(sq[it], rnq[min(4 * it + gq, L - 1)]);
     }
-    // K buffer x & 1 was last read by the update of chunk x - 2
+    // K buffer x & 1 was last read by the update of chunk x - 2.  The K rows
+    // are the operand fragments loaded at the start (lane m + 16 gq holds
+    // columns 32 kq + 8 gq .. + 7 of row 16 b + m), so they are written from
+    // registers rather than read from memory a second time.
     wait_ge(&sm.cnt[CNT_DONE], (unsigned)(x >= 2 ? NSIG * (x - 1) : 0), pc.fault);
 #pragma unroll
-    for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.kb[x & 1][4 * it + gq][swz(4 * it + gq, m * 8)]) = sk[it];
+    for (int b = 0; b < NCT; ++b)
+#pragma unroll
+        for (int kq = 0; kq < 4; ++kq)
+            *reinterpret_cast<uint4*>(&sm.kb[x & 1][16 * b + m][swz(16 * b + m, 32 * kq + 8 * gq)]) = fk[b][kq];
     // V rows of the workgroup's VB columns (VB / 8 lanes per row), loaded into
     // the registers the K rows held, so that their latency overlaps the wait
     // for the Q and V buffers
