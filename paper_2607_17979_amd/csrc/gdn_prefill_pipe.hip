@@ -17,8 +17,9 @@
 //     registers), writes them to its result slot once the state waves are done
 //     with the slot's previous chunk, and finally stages the chunk's K, Q, V
 //     rows into LDS (K double-buffered by chunk parity, Q and V single) once
-//     the state waves have released the buffers: K from the operand registers
-//     it still holds, Q and V read from memory.  A producer therefore has
+//     the state waves have released the buffers: K and the second half of Q
+//     from the operand registers it still holds, the first half of Q and V
+//     read from memory.  A producer therefore has
 //     about four state iterations to prepare a chunk, and none of its latency
 //     is on the state waves' path.
 //
@@ -336,8 +337,8 @@ __device__ __forceinline__ uint4 ld16(const void* base, unsigned byte_off) {
     return *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(base) + byte_off);
 }
 // Streaming load of the V rows (read once), marked non-temporal so that it
-// does not push out of L2 the Q rows that the producers read twice (operand
-// fragments, then staging a few chunks later).
+// does not push out of L2 the Q rows 0..31 of a chunk, which the producers
+// read twice (operand fragments, then staging a few chunks later).
 typedef unsigned u32x4v_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint4 ld16_stream(const void* base, unsigned byte_off) {
     const u32x4v_t r =
@@ -532,14 +533,16 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
     sl.egl[lane] = fast_exp(glast - gx);
     signal(&sm.cnt[CNT_READY0 + pc.pw], lane);
     // ---- stage the chunk's K, Q, V rows once the state waves have
-    //      released the previous chunk's (Q: row 4 it + gq, segment m);
-    //      stream chunk 0 was staged by the whole workgroup
+    //      released the previous chunk's (Q rows 0..31 read again: row 4 it +
+    //      gq, segment m; rows 32..63 are the fragments of block rows 2 and 3
+    //      the scores left in registers); stream chunk 0 was staged by the
+    //      whole workgroup
     if (x == 0) return;
     // (The zero stores before the loads are dead; without them the compiler
     // kept these arrays in scratch memory across the waits below.)
-    uint4 sq[SITEMS];
+    uint4 sq[SITEMS / 2];
 #pragma unroll
-    for (int it = 0; it < SITEMS; ++it) {
+    for (int it = 0; it < SITEMS / 2; ++it) {
         const unsigned off = (unsigned)min(4 * it + gq, L - 1) * qks + 8u * m;
         sq[it] = uint4{0, 0, 0, 0};
         sq[it] = ld16(qc0, 2u * off);
@@ -573,7 +576,12 @@ __device__ __forceinline__ void produce_chunk(SM& sm, const ProdCtx& pc, int x, 
     }
     wait_ge(&sm.cnt[CNT_QVFREE], (unsigned)(NSIG * x), pc.fault);
 #pragma unroll
-    for (int it = 0; it < SITEMS; ++it) *reinterpret_cast<uint4*>(&sm.qb[4 * it + gq][swz(4 * it + gq, m * 8)]) = sq[it];
+    for (int it = 0; it < SITEMS / 2; ++it) *reinterpret_cast<uint4*>(&sm.qb[4 * it + gq][swz(4 * it + gq, m * 8)]) = sq[it];
+#pragma unroll
+    for (int b = 2; b < NCT; ++b)
+#pragma unroll
+        for (int kq = 0; kq < 4; ++kq)
+            *reinterpret_cast<uint4*>(&sm.qb[16 * b + m][swz(16 * b + m, 32 * kq + 8 * gq)]) = fq[b & 1][kq];
 #pragma unroll
     for (int it = 0; it < VIT; ++it)
         *reinterpret_cast<uint4*>(&sm.vb[VRI * it + vr][swz(VRI * it + vr, 8 * vsg)]) = sv[it];
